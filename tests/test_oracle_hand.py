@@ -1,0 +1,97 @@
+"""Oracle pinned to hand-derived cases (tests/golden/).
+
+Every expected value was derived by hand from the paper's definitions (Eq. 1-4,
+Sec. 3.2, Alg. 1), not produced by the oracle.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from golden_io import all_merge_cases, load
+
+
+@pytest.mark.parametrize("name", all_merge_cases())
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_hand_case_stage1(name, dtype):
+    g = load(name)
+    x = oracle.round_to(g["x"], dtype)  # store the inputs in the dtype first
+    res = oracle.merge(x, dtype)
+    assert res.nearest.nb.tolist() == g["nb"]
+    assert res.map.tolist() == g["map"]
+    assert res.count == g["count"]
+    if "clusters" in g:
+        got = [[int(a)] if a == b else [int(a), int(b)] for a, b in zip(res.pairs.src_a, res.pairs.src_b)]
+        assert got == g["clusters"]
+        # Eq. 2: mean of the members, then one rounding to the storage dtype.
+        for k, members in enumerate(g["clusters"]):
+            want = oracle.round_to(x[members].mean(axis=0), dtype)
+            np.testing.assert_array_equal(res.y[k], want)
+
+
+def test_h4_mean_of_first_pair():
+    g = load("h4_all_ties.txt")
+    res = oracle.merge(g["x"], "f32")
+    want = np.zeros(8)
+    want[0] = want[1] = 0.5
+    np.testing.assert_array_equal(res.y[0], want)
+    for k in range(1, 4):
+        np.testing.assert_array_equal(res.y[k], g["x"][k + 1])
+
+
+def test_h5_unmerge_of_merge_is_identity():
+    g = load("h5_dominoes.txt")
+    for dtype in ("f32", "bf16"):
+        x = oracle.round_to(g["x"], dtype)
+        res = oracle.merge(x, dtype)
+        np.testing.assert_array_equal(oracle.unmerge(res.y, res.map), x)
+
+
+def test_h6_two_insertions_compose_and_reconstruct():
+    g = load("h6_blocks.txt")
+    blocks = g["blocks"]
+    stages, rstar, x_up = oracle.schedule(g["x"], "f32", insertions=2)
+    s1, s2 = stages
+    assert s1.nearest.nb.tolist() == g["nb"]
+    assert s1.map.tolist() == g["map"] and s1.count == g["count"]
+    np.testing.assert_array_equal(s1.y, np.stack([blocks[c] for c in g["stage1_rows"]]))
+    assert s2.nearest.nb.tolist() == g["nb2"]
+    assert s2.map.tolist() == g["map2"] and s2.count == g["count2"]
+    np.testing.assert_array_equal(s2.y, np.stack([blocks[c] for c in g["stage2_rows"]]))
+    assert rstar.tolist() == g["rstar"]
+    np.testing.assert_array_equal(x_up, g["x"])
+
+
+def test_compose_small():
+    g = load("compose_small.txt")
+    assert oracle.compose(g["r1"], g["r2"]).tolist() == g["rstar"]
+
+
+def test_h7_raw_dot_would_pair_differently():
+    """Guards the normalisation: the raw dot product prefers (1,2), the cosine (0,2)."""
+    g = load("h7_norms.txt")
+    x = g["x"]
+    raw = x @ x.T
+    np.fill_diagonal(raw, -np.inf)
+    assert np.argmax(raw, axis=1).tolist() == [1, 2, 1]
+    assert oracle.merge(x, "f32").nearest.nb.tolist() == g["nb"]
+
+
+def test_single_token_and_pair():
+    x1 = np.array([[1.0, 2.0, 3.0, 4.0]])
+    r = oracle.merge(x1, "f32")
+    assert r.nearest.nb.tolist() == [-1] and r.map.tolist() == [0] and r.count == 1
+    np.testing.assert_array_equal(r.y, x1)
+    # Any two tokens are each other's only candidate: they always pair.
+    rng = np.random.default_rng(7)
+    for _ in range(20):
+        x2 = rng.standard_normal((2, 6))
+        r = oracle.merge(x2, "f32")
+        assert r.nearest.nb.tolist() == [1, 0] and r.map.tolist() == [0, 0] and r.count == 1
+
+
+def test_zero_token_goes_to_lowest_index():
+    """A zero row has cosine 0 with everything (norm clamped at 1e-12)."""
+    x = np.array([[1.0, 0.0], [0.0, 0.0], [0.5, 0.5], [-1.0, 0.2]])
+    nn = oracle.nearest(x)
+    assert nn.nb[1] == 0
+    assert oracle.cosine(x, 1, 2) == 0.0
