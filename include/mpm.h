@@ -1,0 +1,160 @@
+/*
+ * mpm.h -- C ABI of the Mutual Pair Merging (MPM) token-reduction path,
+ * implemented with hand-written HIP kernels for MI355X (gfx950, CDNA4).
+ *
+ * MPM (arXiv 2604.05718, Sec. 3.2, Alg. 1) reduces the N x D image tokens of a
+ * ViT block input:
+ *   1. normalise each token to unit L2 norm and form the cosine affinity
+ *      S = Xn Xn^T with the diagonal excluded (Eq. 1);
+ *   2. b(i) = argmax_{j != i} S_ij;
+ *   3. keep the mutual pairs (b(b(i)) = i), lower index as representative;
+ *   4. give clusters (pairs and singletons) compact ids r(i) by a
+ *      left-to-right scan (Alg. 1), partners inherit the representative's id;
+ *   5. replace each cluster by the mean of its members (Eq. 2).
+ * Merge maps of successive insertions compose as r*(i) = r2(r1(i)) (Eq. 3),
+ * and the full grid is rebuilt by a gather Z_up[i] = Z[r*(i)] (Eq. 4).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All array pointers are DEVICE pointers owned by the caller. The library
+ *   allocates and frees nothing.
+ * - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *   stream) and never synchronises the host. Counts and offsets stay on the
+ *   device; the caller reads them when it needs them.
+ * - Token rows are D contiguous elements; rows are 16-byte aligned
+ *   (D % 8 == 0 for bfloat16, D % 4 == 0 for float32) and base pointers are
+ *   16-byte aligned.
+ * - A batch holds B images of at most N tokens each. Token rows are either
+ *   DENSE (offsets pointer NULL: image b owns rows [b*N, b*N + N)) or PACKED
+ *   (offsets pointer = device int32[B+1], image b owns rows
+ *   [off[b], off[b+1]), n_b = off[b+1] - off[b] with 1 <= n_b <= N, offsets
+ *   non-decreasing). Packed offsets are data on the device; violating these
+ *   rules is undefined behaviour, not a reported error.
+ * - Per-token integer arrays (nb, map) use a [B][N] slot layout: entry
+ *   b*N + i belongs to token i of image b, for i < n_b. Ids are 0-based and
+ *   image-local.
+ * - Ties: the argmax keeps the lowest index j among equal scores.
+ * - Argument errors are reported synchronously, before anything is launched:
+ *     MPM_ERR_INVALID_ARG  null or misaligned pointer, B < 1, N < 1, D < 1,
+ *                          D not a multiple of 8 (bf16) / 4 (f32), bad dtype;
+ *     MPM_ERR_UNSUPPORTED  N above MPM_MAX_N, B above MPM_MAX_B, D above MPM_MAX_D;
+ *     MPM_ERR_WORKSPACE    workspace smaller than mpm_merge_workspace_bytes;
+ *     MPM_ERR_HIP          a launch failed; mpm_last_hip_error() holds the
+ *                          hipError_t (per host thread).
+ *   Device-side faults surface at the caller's next synchronisation.
+ * - Results are deterministic: the same inputs give bitwise-identical outputs.
+ * - Reentrant: no mutable global state besides the per-thread last HIP error.
+ */
+#ifndef MPM_H
+#define MPM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MPM_OK = 0,
+    MPM_ERR_INVALID_ARG = 1,
+    MPM_ERR_UNSUPPORTED = 2,
+    MPM_ERR_WORKSPACE = 3,
+    MPM_ERR_HIP = 4
+} mpm_status;
+
+typedef enum {
+    MPM_F32 = 0,   /* float32 storage, float32 arithmetic */
+    MPM_BF16 = 1   /* bfloat16 storage, float32 accumulation */
+} mpm_dtype;
+
+#define MPM_MAX_N 16384   /* tokens per image */
+#define MPM_MAX_B 65535   /* images per call */
+#define MPM_MAX_D 16384   /* channels per token */
+
+/* Library version string, e.g. "mpm 0.1.0 gfx950". Never NULL. */
+const char* mpm_version(void);
+
+/* Human-readable name of a status code. Never NULL. */
+const char* mpm_status_string(int status);
+
+/* hipError_t of the last MPM_ERR_HIP returned on this host thread (0 if none). */
+int mpm_last_hip_error(void);
+
+/*
+ * Nearest neighbours (Eq. 1 and the argmax of Sec. 3.2).
+ *   nb[b*N + i] = argmax_{j != i, j < n_b} cos(x_i, x_j), lowest j on equal
+ *                 scores; -1 when n_b == 1.
+ *   best[b*N + i] (optional, may be NULL) = the float32 cosine of that pair.
+ * x: rows of dtype `dt` (dense or packed by x_off). Entries i >= n_b are not
+ * written. Scores are (x_i . x_j) / max(||x_j||, 1e-12) with the dot product
+ * accumulated in float32 from the stored values (bf16 products are exact in
+ * float32); the affinity matrix is never written to memory.
+ */
+int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt,
+               int32_t* nb, float* best, void* stream);
+
+/*
+ * Mutual pairs and compact ids (Sec. 3.2, Alg. 1) from nb.
+ *   map[b*N + i] = r(i) for i < n_b, -1 for n_b <= i < N;
+ *   src[2*(b*N + k)], src[2*(b*N + k) + 1] = (representative, partner) of
+ *     cluster k < count[b] (partner == representative for a singleton);
+ *   count[b] = n'_b, the number of clusters of image b.
+ * x_off: the offsets of the tokens nb was computed on (NULL = dense, n_b = N).
+ */
+int mpm_pair_compact(const int32_t* nb, const int32_t* x_off, int32_t B, int32_t N,
+                     int32_t* map, int32_t* src, int32_t* count, void* stream);
+
+/*
+ * Cluster means (Eq. 2), packed.
+ *   y_off[0] = 0, y_off[b+1] = y_off[b] + count[b];
+ *   y[y_off[b] + k] = mean of the rows src pairs name for cluster k of image b,
+ *     computed in float32 and rounded once (nearest even) to `dt`; a
+ *     singleton is copied bit for bit.
+ * y has room for sum_b count[b] rows (at most B*N). x as in mpm_argmax.
+ */
+int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count,
+                     int32_t B, int32_t N, int32_t D, int32_t dt,
+                     void* y, int32_t* y_off, void* stream);
+
+/* Bytes of device workspace mpm_merge needs (nb, src, count; 256-byte aligned). */
+size_t mpm_merge_workspace_bytes(int32_t B, int32_t N);
+
+/*
+ * One MPM insertion (Alg. 1) = mpm_argmax, mpm_pair_compact and
+ * mpm_pair_average in order on `stream`.
+ *   x, x_off: input tokens (dense or packed);
+ *   y, y_off: merged tokens, packed (capacity B*N rows), offsets int32[B+1];
+ *   map: int32[B*N] merge map in slot layout (-1 beyond n_b);
+ *   ws: device workspace of at least mpm_merge_workspace_bytes(B, N) bytes,
+ *       256-byte aligned. Its layout: nb int32[B*N] at offset 0 (readable
+ *       after the call), then src and count.
+ * Feed (y, y_off) as (x, x_off) of the next insertion.
+ */
+int mpm_merge(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt,
+              void* y, int32_t* y_off, int32_t* map, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Composition of merge maps (Eq. 3): map_ab[b*N + i] = map_b[b*N + map_a[b*N + i]],
+ * or -1 where map_a[b*N + i] < 0. Both maps in slot layout; map_a's values
+ * index image b's entries of map_b. map_ab may alias map_a.
+ */
+int mpm_compose(const int32_t* map_a, const int32_t* map_b, int32_t B, int32_t N,
+                int32_t* map_ab, void* stream);
+
+/*
+ * Gather reconstruction (Eq. 4) with E special rows in front.
+ *   out is dense [B][E + N][D];
+ *   out[b][e]     = z_spec[b][e]                   for e < E (z_spec [B][E][D]; may be NULL iff E == 0);
+ *   out[b][E + i] = z[z_off[b] + map[b*N + i]]     for map >= 0 (bit copy),
+ *                   zeros                          where map < 0.
+ * z, z_off: merged rows, packed (z_off NULL = dense [B][N][D] rows).
+ */
+int mpm_unmerge(const void* z, const int32_t* z_off, const int32_t* map, const void* z_spec, int32_t E,
+                int32_t B, int32_t N, int32_t D, int32_t dt, void* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MPM_H */

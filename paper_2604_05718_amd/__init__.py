@@ -1,0 +1,11 @@
+"""Mutual Pair Merging (MPM) token reduction on MI355X (gfx950).
+
+The computation lives in libmpm.so (hand-written HIP kernels behind the C ABI
+of include/mpm.h); this package is its thin torch binding.
+"""
+from .api import (Merged, ScheduleResult, argmax, compose, merge, pair_average, pair_compact, run_schedule,
+                  unmerge, workspace_bytes)
+from ._lib import MPMError
+
+__all__ = ["Merged", "ScheduleResult", "MPMError", "argmax", "compose", "merge", "pair_average", "pair_compact",
+           "run_schedule", "unmerge", "workspace_bytes"]

@@ -1,0 +1,172 @@
+"""Torch-facing binding of the MPM C ABI.
+
+Argument marshalling only: every step runs in the HIP kernels of libmpm.so,
+on ``torch.cuda.current_stream()``. PyTorch provides device memory and the
+stream. Outputs are allocated at capacity with ``torch.empty``.
+
+Token layouts (see include/mpm.h):
+  dense  -- x is [B, N, D] (or [B*N, D] with N given), x_off None;
+  packed -- x is [R, D] and x_off an int32 device tensor [B+1]; N is the
+            per-image capacity (max tokens of an image).
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+
+import torch
+
+from . import _lib
+
+_DTYPES = {torch.float32: _lib.MPM_F32, torch.bfloat16: _lib.MPM_BF16}
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dt(x: torch.Tensor) -> int:
+    try:
+        return _DTYPES[x.dtype]
+    except KeyError:
+        raise TypeError(f"unsupported token dtype {x.dtype}; use float32 or bfloat16") from None
+
+
+def _rows(x: torch.Tensor, N: int | None, x_off: torch.Tensor | None):
+    """Returns (rows2d, B, N, D) for dense or packed tokens."""
+    if not x.is_cuda:
+        raise ValueError("tokens must be on the GPU")
+    if not x.is_contiguous():
+        raise ValueError("tokens must be contiguous")
+    if x_off is None:
+        if x.dim() == 3:
+            B, n, D = x.shape
+            if N is not None and N != n:
+                raise ValueError("N does not match x.shape[1]")
+            return x.view(B * n, D), B, n, D
+        raise ValueError("dense tokens must be [B, N, D]")
+    if x.dim() != 2 or N is None:
+        raise ValueError("packed tokens are [R, D] with N given")
+    if x_off.dtype != torch.int32 or not x_off.is_cuda:
+        raise ValueError("x_off must be an int32 device tensor [B+1]")
+    return x, x_off.numel() - 1, int(N), x.shape[1]
+
+
+def argmax(x, x_off=None, N=None, with_best=False):
+    """nb [B, N] int32 (and best [B, N] float32 cosines when ``with_best``)."""
+    x2, B, N, D = _rows(x, N, x_off)
+    nb = torch.empty((B, N), dtype=torch.int32, device=x.device)
+    best = torch.empty((B, N), dtype=torch.float32, device=x.device) if with_best else None
+    lib = _lib.load()
+    _lib.check("mpm_argmax", lib.mpm_argmax(_p(x2), _p(x_off), B, N, D, _dt(x), _p(nb), _p(best), _stream()))
+    return (nb, best) if with_best else nb
+
+
+def pair_compact(nb, x_off=None):
+    """(map [B, N], src [B, N, 2], count [B]) from nb [B, N]."""
+    B, N = nb.shape
+    dev = nb.device
+    m = torch.empty((B, N), dtype=torch.int32, device=dev)
+    src = torch.empty((B, N, 2), dtype=torch.int32, device=dev)
+    count = torch.empty((B,), dtype=torch.int32, device=dev)
+    lib = _lib.load()
+    _lib.check("mpm_pair_compact", lib.mpm_pair_compact(_p(nb.contiguous()), _p(x_off), B, N, _p(m), _p(src),
+                                                        _p(count), _stream()))
+    return m, src, count
+
+
+def pair_average(x, src, count, x_off=None, N=None):
+    """(y [B*N, D] packed at capacity, y_off [B+1]) cluster means."""
+    x2, B, N, D = _rows(x, N, x_off)
+    y = torch.empty((B * N, D), dtype=x.dtype, device=x.device)
+    y_off = torch.empty((B + 1,), dtype=torch.int32, device=x.device)
+    lib = _lib.load()
+    _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(x2), _p(x_off), _p(src), _p(count), B, N, D, _dt(x),
+                                                        _p(y), _p(y_off), _stream()))
+    return y, y_off
+
+
+def workspace_bytes(B: int, N: int) -> int:
+    return int(_lib.load().mpm_merge_workspace_bytes(B, N))
+
+
+@dataclass
+class Merged:
+    y: torch.Tensor       # [B*N, D] packed merged tokens (rows beyond y_off[B] unused)
+    y_off: torch.Tensor   # [B+1] int32
+    map: torch.Tensor     # [B, N] int32, -1 beyond n_b
+    ws: torch.Tensor      # workspace; nb lives at its start
+    B: int
+    N: int
+
+    @property
+    def nb(self) -> torch.Tensor:
+        return self.ws[: self.B * self.N * 4].view(torch.int32).view(self.B, self.N)
+
+
+def merge(x, x_off=None, N=None, ws=None) -> Merged:
+    """One MPM insertion (Alg. 1)."""
+    x2, B, N, D = _rows(x, N, x_off)
+    dev = x.device
+    need = workspace_bytes(B, N)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty((need,), dtype=torch.uint8, device=dev)
+    y = torch.empty((B * N, D), dtype=x.dtype, device=dev)
+    y_off = torch.empty((B + 1,), dtype=torch.int32, device=dev)
+    m = torch.empty((B, N), dtype=torch.int32, device=dev)
+    lib = _lib.load()
+    _lib.check("mpm_merge", lib.mpm_merge(_p(x2), _p(x_off), B, N, D, _dt(x), _p(y), _p(y_off), _p(m), _p(ws),
+                                          ws.numel(), _stream()))
+    return Merged(y, y_off, m, ws, B, N)
+
+
+def compose(map_a, map_b, out=None):
+    """r*(i) = map_b[map_a[i]] per image (Eq. 3); maps [B, N] int32."""
+    B, N = map_a.shape
+    out = torch.empty_like(map_a) if out is None else out
+    lib = _lib.load()
+    _lib.check("mpm_compose", lib.mpm_compose(_p(map_a), _p(map_b.contiguous()), B, N, _p(out), _stream()))
+    return out
+
+
+def unmerge(z, z_off, rmap, z_spec=None, out=None):
+    """Dense [B, E+N, D] grid: E special rows, then z[z_off[b] + rmap[b, i]] (Eq. 4)."""
+    B, N = rmap.shape
+    if z.dim() == 3:
+        z = z.reshape(-1, z.shape[-1])
+    D = z.shape[1]
+    E = 0 if z_spec is None else z_spec.shape[1]
+    if out is None:
+        out = torch.empty((B, E + N, D), dtype=z.dtype, device=z.device)
+    lib = _lib.load()
+    _lib.check("mpm_unmerge", lib.mpm_unmerge(_p(z), _p(z_off), _p(rmap), _p(z_spec), E, B, N, D, _dt(z), _p(out),
+                                              _stream()))
+    return out
+
+
+@dataclass
+class ScheduleResult:
+    stages: list          # Merged per insertion
+    rstar: torch.Tensor   # composed map [B, N]
+    out: torch.Tensor     # reconstructed grid [B, N, D]
+
+
+def run_schedule(x, insertions: int = 2, workspaces=None) -> ScheduleResult:
+    """Insertions with identity blocks in between (Sec. 3.3), composed maps
+    (Eq. 3) and one gather back to the full grid (Eq. 4)."""
+    B, N, D = x.shape
+    stages = []
+    cur, cur_off = x, None
+    rstar = None
+    for s in range(insertions):
+        ws = None if workspaces is None else workspaces[s]
+        m = merge(cur, cur_off, N=N, ws=ws)
+        stages.append(m)
+        rstar = m.map if rstar is None else compose(rstar, m.map)
+        cur, cur_off = m.y, m.y_off
+    out = unmerge(cur, cur_off, rstar)
+    return ScheduleResult(stages, rstar, out)

@@ -1,0 +1,165 @@
+// C ABI of the MPM library: argument validation (pure host code, run before
+// anything touches the GPU), workspace carving and kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "../../include/mpm.h"
+#include "mpm_launch.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+int hip_status(hipError_t e)
+{
+    if (e == hipSuccess) return MPM_OK;
+    g_last_hip_error = static_cast<int>(e);
+    return MPM_ERR_HIP;
+}
+
+int check_shape(int32_t B, int32_t N)
+{
+    if (B < 1 || N < 1) return MPM_ERR_INVALID_ARG;
+    if (B > MPM_MAX_B || N > MPM_MAX_N) return MPM_ERR_UNSUPPORTED;
+    return MPM_OK;
+}
+
+int check_rows(int32_t B, int32_t N, int32_t D, int32_t dt)
+{
+    const int s = check_shape(B, N);
+    if (s != MPM_OK) return s;
+    if (dt != MPM_F32 && dt != MPM_BF16) return MPM_ERR_INVALID_ARG;
+    if (D < 1) return MPM_ERR_INVALID_ARG;
+    if (D % (dt == MPM_BF16 ? 8 : 4) != 0) return MPM_ERR_INVALID_ARG;  // 16-byte rows
+    if (D > MPM_MAX_D) return MPM_ERR_UNSUPPORTED;
+    return MPM_OK;
+}
+
+bool ok_rows_ptr(const void* p) { return p != nullptr && aligned(p, 16); }
+bool ok_int_ptr(const void* p) { return p != nullptr && aligned(p, 4); }
+bool ok_opt_int_ptr(const void* p) { return p == nullptr || aligned(p, 4); }
+
+constexpr size_t kAlign = 256;
+size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct MergeWorkspace {
+    int32_t* nb;
+    int32_t* src;
+    int32_t* count;
+};
+
+size_t workspace_bytes(int32_t B, int32_t N, MergeWorkspace* ws, void* base)
+{
+    const size_t slots = (size_t)B * (size_t)N;
+    const size_t nb_bytes = round_up(slots * sizeof(int32_t));
+    const size_t src_bytes = round_up(2 * slots * sizeof(int32_t));
+    const size_t cnt_bytes = round_up((size_t)B * sizeof(int32_t));
+    if (ws) {
+        char* p = static_cast<char*>(base);
+        ws->nb = reinterpret_cast<int32_t*>(p);
+        ws->src = reinterpret_cast<int32_t*>(p + nb_bytes);
+        ws->count = reinterpret_cast<int32_t*>(p + nb_bytes + src_bytes);
+    }
+    return nb_bytes + src_bytes + cnt_bytes;
+}
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+const char* mpm_version(void) { return "mpm 0.1.0 gfx950"; }
+
+const char* mpm_status_string(int status)
+{
+    switch (status) {
+    case MPM_OK: return "MPM_OK";
+    case MPM_ERR_INVALID_ARG: return "MPM_ERR_INVALID_ARG";
+    case MPM_ERR_UNSUPPORTED: return "MPM_ERR_UNSUPPORTED";
+    case MPM_ERR_WORKSPACE: return "MPM_ERR_WORKSPACE";
+    case MPM_ERR_HIP: return "MPM_ERR_HIP";
+    default: return "MPM_UNKNOWN_STATUS";
+    }
+}
+
+int mpm_last_hip_error(void) { return g_last_hip_error; }
+
+int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* nb,
+               float* best, void* stream)
+{
+    const int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(nb) || !ok_opt_int_ptr(best))
+        return MPM_ERR_INVALID_ARG;
+    return hip_status(mpm::launch_argmax(x, x_off, B, N, D, dt, nb, best, as_stream(stream)));
+}
+
+int mpm_pair_compact(const int32_t* nb, const int32_t* x_off, int32_t B, int32_t N, int32_t* map, int32_t* src,
+                     int32_t* count, void* stream)
+{
+    const int s = check_shape(B, N);
+    if (s != MPM_OK) return s;
+    if (!ok_int_ptr(nb) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(map) || !ok_int_ptr(src) || !ok_int_ptr(count))
+        return MPM_ERR_INVALID_ARG;
+    return hip_status(mpm::launch_pair_compact(nb, x_off, B, N, map, src, count, as_stream(stream)));
+}
+
+int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count, int32_t B,
+                     int32_t N, int32_t D, int32_t dt, void* y, int32_t* y_off, void* stream)
+{
+    const int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(src) || !ok_int_ptr(count) || !ok_rows_ptr(y) ||
+        !ok_int_ptr(y_off))
+        return MPM_ERR_INVALID_ARG;
+    return hip_status(mpm::launch_pair_average(x, x_off, src, count, B, N, D, dt, y, y_off, as_stream(stream)));
+}
+
+size_t mpm_merge_workspace_bytes(int32_t B, int32_t N)
+{
+    if (B < 1 || N < 1) return 0;
+    return workspace_bytes(B, N, nullptr, nullptr);
+}
+
+int mpm_merge(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* y,
+              int32_t* y_off, int32_t* map, void* ws, size_t ws_bytes, void* stream)
+{
+    const int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_rows_ptr(y) || !ok_int_ptr(y_off) || !ok_int_ptr(map) ||
+        ws == nullptr || !aligned(ws, kAlign))
+        return MPM_ERR_INVALID_ARG;
+    MergeWorkspace w;
+    if (ws_bytes < workspace_bytes(B, N, &w, ws)) return MPM_ERR_WORKSPACE;
+    const hipStream_t st = as_stream(stream);
+    hipError_t e = mpm::launch_argmax(x, x_off, B, N, D, dt, w.nb, nullptr, st);
+    if (e == hipSuccess) e = mpm::launch_pair_compact(w.nb, x_off, B, N, map, w.src, w.count, st);
+    if (e == hipSuccess) e = mpm::launch_pair_average(x, x_off, w.src, w.count, B, N, D, dt, y, y_off, st);
+    return hip_status(e);
+}
+
+int mpm_compose(const int32_t* map_a, const int32_t* map_b, int32_t B, int32_t N, int32_t* map_ab, void* stream)
+{
+    const int s = check_shape(B, N);
+    if (s != MPM_OK) return s;
+    if (!ok_int_ptr(map_a) || !ok_int_ptr(map_b) || !ok_int_ptr(map_ab)) return MPM_ERR_INVALID_ARG;
+    return hip_status(mpm::launch_compose(map_a, map_b, B, N, map_ab, as_stream(stream)));
+}
+
+int mpm_unmerge(const void* z, const int32_t* z_off, const int32_t* map, const void* z_spec, int32_t E, int32_t B,
+                int32_t N, int32_t D, int32_t dt, void* out, void* stream)
+{
+    const int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (E < 0 || (E > 0 && !ok_rows_ptr(z_spec)) || (E == 0 && z_spec != nullptr && !aligned(z_spec, 16)))
+        return MPM_ERR_INVALID_ARG;
+    if ((long)E + N > MPM_MAX_N + (long)MPM_MAX_N) return MPM_ERR_UNSUPPORTED;
+    if (!ok_rows_ptr(z) || !ok_opt_int_ptr(z_off) || !ok_int_ptr(map) || !ok_rows_ptr(out)) return MPM_ERR_INVALID_ARG;
+    return hip_status(mpm::launch_unmerge(z, z_off, map, z_spec, E, B, N, D, dt, out, as_stream(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,29 @@
+// Host-side launchers of the MPM kernels. Arguments are validated by the
+// C ABI layer before any of these is called; each returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mpm {
+
+enum Dtype : int { kF32 = 0, kBf16 = 1 };
+
+hipError_t launch_argmax(const void* x, const int32_t* x_off, int B, int N, int D, int dt,
+                         int32_t* nb, float* best, hipStream_t stream);
+
+hipError_t launch_pair_compact(const int32_t* nb, const int32_t* x_off, int B, int N,
+                               int32_t* map, int32_t* src, int32_t* count, hipStream_t stream);
+
+hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_t* src,
+                               const int32_t* count, int B, int N, int D, int dt, void* y,
+                               int32_t* y_off, hipStream_t stream);
+
+hipError_t launch_compose(const int32_t* map_a, const int32_t* map_b, int B, int N,
+                          int32_t* map_ab, hipStream_t stream);
+
+hipError_t launch_unmerge(const void* z, const int32_t* z_off, const int32_t* map,
+                          const void* z_spec, int E, int B, int N, int D, int dt, void* out,
+                          hipStream_t stream);
+
+}  // namespace mpm

@@ -1,0 +1,177 @@
+// HBM-streaming steps of MPM for gfx950: cluster means (Eq. 2), map
+// composition (Eq. 3) and gather reconstruction (Eq. 4).
+//
+// The row kernels treat a token row as D*s/16 independent 16-byte vectors and
+// give every lane one vector at a time, so any D keeps all lanes busy and
+// every global access is a 16-byte, fully coalesced load or store. Output rows
+// are written once and never re-read by the kernel, so they are stored with
+// non-temporal hints.
+#include "mpm_device.h"
+#include "mpm_launch.h"
+
+namespace mpm {
+namespace {
+
+constexpr int kRowThreads = 256;
+constexpr int kRowBytesPerBlock = 32768;  // output bytes one workgroup handles
+
+// Walks the flat range [f0, f1) of 16-byte vectors of a row-major block whose
+// rows hold `vpr` vectors, calling body(row, vec) with a stride of the
+// workgroup size; row/column advance incrementally (no per-element division).
+template <class Body>
+__device__ __forceinline__ void for_each_vec(long f0, long f1, int vpr, Body body)
+{
+    const int t = threadIdx.x;
+    long f = f0 + t;
+    if (f >= f1) return;
+    long row = f / vpr;
+    int col = (int)(f - row * vpr);
+    const int step_rows = kRowThreads / vpr;
+    const int step_cols = kRowThreads - step_rows * vpr;
+    for (; f < f1; f += kRowThreads) {
+        body(row, col);
+        row += step_rows;
+        col += step_cols;
+        if (col >= vpr) {
+            col -= vpr;
+            row += 1;
+        }
+    }
+}
+
+// Sum of count[0..b) by the first wave; broadcast through LDS.
+__device__ __forceinline__ int image_offset(const int32_t* count, int b)
+{
+    __shared__ int off_sh;
+    if (threadIdx.x < kWave) {
+        int s = 0;
+        for (int k = threadIdx.x; k < b; k += kWave) s += count[k];
+        s = wave_sum(s);
+        if (threadIdx.x == 0) off_sh = s;
+    }
+    __syncthreads();
+    return off_sh;
+}
+
+template <class S>
+__global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
+    const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, const int32_t* __restrict__ src,
+    const int32_t* __restrict__ count, int N, int D, int rows_per_block, uint8_t* __restrict__ y,
+    int32_t* __restrict__ y_off)
+{
+    const int b = blockIdx.y;
+    const int off = image_offset(count, b);
+    const int cnt = count[b];
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        y_off[b + 1] = off + cnt;
+        if (b == 0) y_off[0] = 0;
+    }
+    const int k0 = blockIdx.x * rows_per_block;
+    const int k1 = min(cnt, k0 + rows_per_block);
+    if (k0 >= k1) return;
+    const long rowbytes = (long)D * S::kBytes;
+    const int vpr = (int)(rowbytes / 16);
+    const uint8_t* ximg = x + (long)(x_off ? x_off[b] : b * N) * rowbytes;
+    uint8_t* yimg = y + (long)off * rowbytes;
+    const int32_t* srcb = src + 2L * b * N;
+    for_each_vec((long)k0 * vpr, (long)k1 * vpr, vpr, [&](long k, int c) {
+        const int ia = srcb[2 * k];
+        const int ib = srcb[2 * k + 1];
+        const u32x4 va = load16(ximg + ia * rowbytes + c * 16);
+        u32x4 out = va;  // a singleton is copied bit for bit
+        if (ib != ia) out = mean16(va, load16(ximg + ib * rowbytes + c * 16), S{});
+        store16_stream(yimg + k * rowbytes + c * 16, out);
+    });
+}
+
+__global__ __launch_bounds__(kRowThreads) void compose_kernel(const int32_t* map_a,
+                                                              const int32_t* __restrict__ map_b, int N,
+                                                              long total, int32_t* map_ab)
+{
+    const long t = (long)blockIdx.x * kRowThreads + threadIdx.x;
+    if (t >= total) return;
+    const long b = t / N;
+    const int a = map_a[t];
+    map_ab[t] = a < 0 ? -1 : map_b[b * N + a];
+}
+
+template <class S>
+__global__ __launch_bounds__(kRowThreads) void unmerge_kernel(
+    const uint8_t* __restrict__ z, const int32_t* __restrict__ z_off, const int32_t* __restrict__ map,
+    const uint8_t* __restrict__ z_spec, int E, int N, int D, int rows_per_block, uint8_t* __restrict__ out)
+{
+    const int b = blockIdx.y;
+    const int rows = E + N;
+    const int r0 = blockIdx.x * rows_per_block;
+    const int r1 = min(rows, r0 + rows_per_block);
+    if (r0 >= r1) return;
+    const long rowbytes = (long)D * S::kBytes;
+    const int vpr = (int)(rowbytes / 16);
+    const uint8_t* zimg = z + (long)(z_off ? z_off[b] : b * N) * rowbytes;
+    const int32_t* mapb = map + (long)b * N;
+    uint8_t* oimg = out + (long)b * rows * rowbytes;
+    for_each_vec((long)r0 * vpr, (long)r1 * vpr, vpr, [&](long r, int c) {
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (r < E) {
+            v = load16(z_spec + ((long)b * E + r) * rowbytes + c * 16);
+        } else {
+            const int m = mapb[r - E];
+            if (m >= 0) v = load16(zimg + m * rowbytes + c * 16);
+        }
+        store16_stream(oimg + r * rowbytes + c * 16, v);
+    });
+}
+
+int rows_per_block_for(long rowbytes)
+{
+    const long r = kRowBytesPerBlock / rowbytes;
+    return r < 1 ? 1 : (int)r;
+}
+
+}  // namespace
+
+hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count,
+                               int B, int N, int D, int dt, void* y, int32_t* y_off, hipStream_t stream)
+{
+    const long rowbytes = (long)D * (dt == kBf16 ? 2 : 4);
+    const int rpb = rows_per_block_for(rowbytes);
+    dim3 grid((N + rpb - 1) / rpb, B);
+    const uint8_t* xp = static_cast<const uint8_t*>(x);
+    uint8_t* yp = static_cast<uint8_t*>(y);
+    if (dt == kBf16)
+        hipLaunchKernelGGL(pair_average_kernel<Bf16>, grid, dim3(kRowThreads), 0, stream, xp, x_off, src, count, N, D,
+                           rpb, yp, y_off);
+    else
+        hipLaunchKernelGGL(pair_average_kernel<F32>, grid, dim3(kRowThreads), 0, stream, xp, x_off, src, count, N, D,
+                           rpb, yp, y_off);
+    return hipGetLastError();
+}
+
+hipError_t launch_compose(const int32_t* map_a, const int32_t* map_b, int B, int N, int32_t* map_ab,
+                          hipStream_t stream)
+{
+    const long total = (long)B * N;
+    dim3 grid((unsigned)((total + kRowThreads - 1) / kRowThreads));
+    hipLaunchKernelGGL(compose_kernel, grid, dim3(kRowThreads), 0, stream, map_a, map_b, N, total, map_ab);
+    return hipGetLastError();
+}
+
+hipError_t launch_unmerge(const void* z, const int32_t* z_off, const int32_t* map, const void* z_spec, int E, int B,
+                          int N, int D, int dt, void* out, hipStream_t stream)
+{
+    const long rowbytes = (long)D * (dt == kBf16 ? 2 : 4);
+    const int rpb = rows_per_block_for(rowbytes);
+    dim3 grid((E + N + rpb - 1) / rpb, B);
+    const uint8_t* zp = static_cast<const uint8_t*>(z);
+    const uint8_t* sp = static_cast<const uint8_t*>(z_spec);
+    uint8_t* op = static_cast<uint8_t*>(out);
+    if (dt == kBf16)
+        hipLaunchKernelGGL(unmerge_kernel<Bf16>, grid, dim3(kRowThreads), 0, stream, zp, z_off, map, sp, E, N, D, rpb,
+                           op);
+    else
+        hipLaunchKernelGGL(unmerge_kernel<F32>, grid, dim3(kRowThreads), 0, stream, zp, z_off, map, sp, E, N, D, rpb,
+                           op);
+    return hipGetLastError();
+}
+
+}  // namespace mpm

@@ -1,0 +1,81 @@
+"""C ABI checks that need no GPU: the library loads, exports every function the
+header declares, and rejects bad arguments synchronously before any launch."""
+import ctypes
+
+import pytest
+
+from paper_2604_05718_amd import _lib
+
+A = ctypes.c_void_p(0x10000)       # stand-in device pointers: never dereferenced,
+A2 = ctypes.c_void_p(0x20000)      # the calls below return before any launch
+MIS = ctypes.c_void_p(0x10004)     # 4-byte aligned, not 16-byte aligned
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def test_exports_every_header_function(lib):
+    names = _lib.header_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in _lib.SIGNATURES, n
+
+
+def test_version_and_status_strings(lib):
+    assert b"gfx950" in lib.mpm_version()
+    assert lib.mpm_status_string(0) == b"MPM_OK"
+    assert lib.mpm_status_string(3) == b"MPM_ERR_WORKSPACE"
+    assert lib.mpm_status_string(99) == b"MPM_UNKNOWN_STATUS"
+    assert lib.mpm_last_hip_error() == 0
+
+
+def test_workspace_bytes(lib):
+    B, N = 64, 1024
+    r = lambda v: (v + 255) // 256 * 256
+    assert lib.mpm_merge_workspace_bytes(B, N) == r(4 * B * N) + r(8 * B * N) + r(4 * B)
+    assert lib.mpm_merge_workspace_bytes(0, 5) == 0
+
+
+@pytest.mark.parametrize("args,code", [
+    ((A, None, 0, 16, 64, 1, A2, None), 1),         # B < 1
+    ((A, None, 2, 0, 64, 1, A2, None), 1),          # N < 1
+    ((A, None, 2, 16, 0, 1, A2, None), 1),          # D < 1
+    ((A, None, 2, 16, 12, 1, A2, None), 1),         # bf16 rows not 16-byte multiples
+    ((A, None, 2, 16, 6, 0, A2, None), 1),          # f32 rows not 16-byte multiples
+    ((A, None, 2, 16, 64, 7, A2, None), 1),         # unknown dtype
+    ((None, None, 2, 16, 64, 1, A2, None), 1),      # null tokens
+    ((MIS, None, 2, 16, 64, 1, A2, None), 1),       # misaligned tokens
+    ((A, None, 2, 16, 64, 1, None, None), 1),       # null nb
+    ((A, None, 2, 16384 + 1, 64, 1, A2, None), 2),  # N above MPM_MAX_N
+    ((A, None, 65536, 16, 64, 1, A2, None), 2),     # B above MPM_MAX_B
+    ((A, None, 2, 16, 16384 + 8, 1, A2, None), 2),  # D above MPM_MAX_D
+])
+def test_argmax_rejects(lib, args, code):
+    assert lib.mpm_argmax(*args, None) == code
+
+
+def test_merge_rejects(lib):
+    need = lib.mpm_merge_workspace_bytes(4, 64)
+    ok = (A, None, 4, 64, 64, 1, A2, A2, A2, A, need)
+    # Workspace one byte short.
+    assert lib.mpm_merge(*ok[:10], need - 1, None) == 3
+    # Workspace not 256-byte aligned.
+    assert lib.mpm_merge(*ok[:9], ctypes.c_void_p(0x10010), need, None) == 1
+    assert lib.mpm_merge(*ok[:9], None, need, None) == 1
+    # Null merged-token buffer.
+    assert lib.mpm_merge(A, None, 4, 64, 64, 1, None, A2, A2, A, need, None) == 1
+
+
+def test_other_entry_points_reject(lib):
+    assert lib.mpm_pair_compact(A, None, 0, 8, A, A, A, None) == 1
+    assert lib.mpm_pair_compact(None, None, 2, 8, A, A, A, None) == 1
+    assert lib.mpm_pair_average(A, None, A, A, 2, 8, 64, 1, MIS, A, None) == 1
+    assert lib.mpm_compose(A, None, 2, 8, A, None) == 1
+    assert lib.mpm_compose(A, A, 2, 16385, A, None) == 2
+    assert lib.mpm_unmerge(A, None, A, None, -1, 2, 8, 64, 1, A, None) == 1   # E < 0
+    assert lib.mpm_unmerge(A, None, A, None, 2, 2, 8, 64, 1, A, None) == 1    # E > 0 needs z_spec
+    assert lib.mpm_unmerge(A, None, A, None, 0, 2, 8, 64, 1, None, None) == 1
+    assert lib.mpm_last_hip_error() == 0
