@@ -44,8 +44,10 @@ struct Mfma<Bf16> {
     {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            bf16x2 v = __builtin_bit_cast(bf16x2, a[e]);
-            s = __builtin_amdgcn_fdot2_f32_bf16(v, v, s, false);
+            const float lo = bf16_lo(a[e]);
+            const float hi = bf16_hi(a[e]);
+            s = fmaf(lo, lo, s);
+            s = fmaf(hi, hi, s);
         }
         return s;
     }
