@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""MPM merge + unmerge throughput on one MI355X.
+
+One step = the whole hot path over one batch already resident in HBM: MPM
+before encoder blocks 2 and 5 (two insertions, identity blocks in between),
+map composition and the gather back to the full token grid. Default workload:
+ViT-B/16 tokens of 512x512 images (B=64, N=1024, D=768, bfloat16), synthetic.
+
+Prints one JSON line: images/s, per-step time, the roofline of the dominant
+kernel (the fused affinity-argmax, MFMA-bound), per-kernel timings, and the
+CPU oracle timed on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 matrix
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak"
+
+# HBM traffic of the affinity-argmax kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
+# runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
+# the kernel source it was measured on.
+TRAFFIC = None  # {"source_sha256": ..., "bytes_per_launch": ...}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    p = os.path.join(ROOT, "paper_2604_05718_amd", "csrc", "affinity_argmax.hip")
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()
+
+
+def algorithmic_work(cfg, counts):
+    """Per kernel of one step: ('flops'|'bytes', amount). counts[s] = per-image
+    token counts after insertion s (counts[-1] = N for every image)."""
+    s = 2 if cfg.dtype == "bf16" else 4
+    D, N, B = cfg.D, cfg.N, cfg.B
+    work = []
+    n_in = [N] * B
+    for st in range(cfg.insertions):
+        n_out = counts[st]
+        work.append(("flops", sum(2.0 * n * n * D for n in n_in)))
+        # compact: read nb (4n), write map (4N) and src (8n'), count (4)
+        work.append(("bytes", sum(4.0 * n + 4.0 * N + 8.0 * m + 4 for n, m in zip(n_in, n_out))))
+        # average: read every member row once, write every cluster row, read src
+        work.append(("bytes", sum((n + m) * D * s + 8.0 * m for n, m in zip(n_in, n_out))))
+        n_in = n_out
+    if cfg.insertions == 1:
+        work.append(("bytes", 8.0 * N * B))
+    else:
+        # compose: read r* (4N), touch the stage map of the previous survivors (4 n), write r* (4N)
+        for st in range(1, cfg.insertions):
+            work.append(("bytes", sum(8.0 * N + 4.0 * m for m in counts[st - 1])))
+    # gather: read the composed map, each final row once, write the full grid
+    work.append(("bytes", sum(4.0 * N + m * D * s + N * D * s for m in n_in)))
+    return work
+
+
+def cpu_baseline(cfg, x_cpu, budget_s: float):
+    import oracle
+
+    threads = oracle.default_threads()
+    t0 = time.perf_counter()
+    done = 0
+    for b in range(cfg.B):
+        oracle.schedule(oracle.as_f64(x_cpu[b]), cfg.dtype, insertions=cfg.insertions, threads=threads)
+        done += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {
+        "value": done / el,
+        "unit": "images/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"first {done} of {cfg.B} images of {cfg.name}, full schedule ({cfg.insertions} insertions, "
+                   f"compose, gather), float64 brute force, {el:.1f} s"),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default="vit_b_512")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="budget of the CPU oracle baseline (0 skips it)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        log("bench.py: this build measures one GPU only; the path shards by image with no communication, "
+            "so a multi-GPU figure is not produced. Run with --gpus 1.")
+        return 2
+
+    import torch
+
+    import paper_2604_05718_amd as mpm  # noqa: F401  (fails loudly without libmpm.so)
+    from paper_2604_05718_amd import api, synth
+
+    cfg = synth.config(args.workload)
+    dev = torch.device("cuda:0")
+    dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    log(f"bench: {cfg.name} B={cfg.B} N={cfg.N} D={cfg.D} {cfg.dtype}, generating inputs")
+    x_cpu = synth.make_batch(cfg, seed=0)
+    x = x_cpu.to(dev)
+    sched = api.Schedule(cfg.B, cfg.N, cfg.D, dtype, cfg.insertions)
+
+    for _ in range(args.warmup):
+        sched.run(x)
+    torch.cuda.synchronize()
+    log(f"bench: warmup {args.warmup} done, timing {args.steps} steps")
+
+    nm = sched.n_marks()
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(nm)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for k in range(args.steps):
+        sched.run(x, marks[k])
+    end.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / args.steps
+
+    # Same loop without per-kernel events, to show what they cost.
+    start2, end2 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start2.record()
+    for k in range(args.steps):
+        sched.run(x)
+    end2.record()
+    torch.cuda.synchronize()
+    ms_plain = start2.elapsed_time(end2) / args.steps
+
+    names = sched.kernel_names
+    per_kernel_ms = [sum(m[i].elapsed_time(m[i + 1]) for m in marks) / args.steps for i in range(len(names))]
+    counts = [torch.diff(sched.y_off[s].cpu()).tolist() for s in range(cfg.insertions)]
+    work = algorithmic_work(cfg, counts)
+
+    kernels = []
+    for name, ms, (kind, amount) in zip(names, per_kernel_ms, work):
+        ent = {"name": name, "us": round(ms * 1e3, 2)}
+        if kind == "flops":
+            tf = amount / (ms * 1e-3) / 1e12
+            peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
+            ent.update({"gflop": round(amount / 1e9, 3), "tflops": round(tf, 1), "frac_mfma": round(tf / peak, 4)})
+        else:
+            gbs = amount / (ms * 1e-3) / 1e9
+            ent.update({"mbytes": round(amount / 1e6, 3), "gbs": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
+        kernels.append(ent)
+
+    # Dominant kernel: the fused affinity-argmax (both insertions' launches).
+    a_idx = [i for i, n in enumerate(names) if n.startswith("argmax")]
+    a_flops = sum(work[i][1] for i in a_idx)
+    a_ms = sum(per_kernel_ms[i] for i in a_idx)
+    peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
+    achieved = a_flops / len(a_idx) / (a_ms / len(a_idx) * 1e-3) / 1e12
+    traffic = None
+    if TRAFFIC and TRAFFIC.get("source_sha256") == kernel_source_hash():
+        traffic = TRAFFIC["bytes_per_launch"]
+    roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": traffic}
+
+    value = cfg.B / (ms_per_step * 1e-3)
+    result = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": (f"{cfg.name}: ViT token grid {cfg.G}x{cfg.G} (N={cfg.N}), D={cfg.D}, B={cfg.B}, "
+                                f"{cfg.insertions} MPM insertions + compose + gather"),
+                   "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "none (1 GPU)"},
+        "tokens_per_s": round(value * cfg.N, 0),
+        "ms_per_step_without_kernel_events": round(ms_plain, 4),
+        "survivors_mean": [round(sum(c) / len(c), 1) for c in counts],
+        "roofline": roofline,
+        "kernels": kernels,
+    }
+    if args.cpu_seconds > 0:
+        log("bench: timing the CPU oracle baseline")
+        result["cpu_baseline"] = cpu_baseline(cfg, x_cpu, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

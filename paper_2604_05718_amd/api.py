@@ -170,3 +170,85 @@ def run_schedule(x, insertions: int = 2, workspaces=None) -> ScheduleResult:
         cur, cur_off = m.y, m.y_off
     out = unmerge(cur, cur_off, rstar)
     return ScheduleResult(stages, rstar, out)
+
+
+class Schedule:
+    """Preallocated MPM schedule for a fixed batch shape: every buffer is
+    allocated once, so ``run`` only launches kernels (no allocation, no host
+    synchronisation). Stage s consumes stage s-1's packed output (Sec. 3.3);
+    the composed map and the reconstruction follow (Eq. 3, Eq. 4).
+
+    ``run(x, marks=None)``: when ``marks`` is a list of ``n_marks()``
+    torch.cuda.Event objects, event k is recorded on the current stream just
+    before kernel k (in ``kernel_names`` order) and the last one after the
+    gather, so consecutive events bracket single kernels."""
+
+    def __init__(self, B: int, N: int, D: int, dtype: torch.dtype, insertions: int = 2, device="cuda"):
+        if insertions < 1:
+            raise ValueError("at least one insertion")
+        self.B, self.N, self.D, self.dtype, self.insertions = B, N, D, dtype, insertions
+        dev = torch.device(device)
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.nb = [torch.empty((B, N), **i32) for _ in range(insertions)]
+        self.src = [torch.empty((B, N, 2), **i32) for _ in range(insertions)]
+        self.count = [torch.empty((B,), **i32) for _ in range(insertions)]
+        self.map = [torch.empty((B, N), **i32) for _ in range(insertions)]
+        self.y = [torch.empty((B * N, D), dtype=dtype, device=dev) for _ in range(insertions)]
+        self.y_off = [torch.empty((B + 1,), **i32) for _ in range(insertions)]
+        self.rstar = torch.empty((B, N), **i32)
+        self.out = torch.empty((B, N, D), dtype=dtype, device=dev)
+        self._lib = _lib.load()
+        self._dt = _DTYPES[dtype]
+
+    @property
+    def kernel_names(self) -> list:
+        names = []
+        for s in range(self.insertions):
+            names += [f"argmax{s + 1}", f"compact{s + 1}", f"average{s + 1}"]
+        names += ["compose"] * max(0, self.insertions - 1) + ["unmerge"]
+        if self.insertions == 1:
+            names.insert(len(names) - 1, "copy_map")
+        return names
+
+    def run(self, x: torch.Tensor, marks=None) -> torch.Tensor:
+        if x.shape != (self.B, self.N, self.D) or x.dtype != self.dtype or not x.is_contiguous():
+            raise ValueError("input does not match the schedule's shape/dtype")
+        lib, st, B, N, D, dt = self._lib, _stream(), self.B, self.N, self.D, self._dt
+        k = 0
+
+        def mark():
+            nonlocal k
+            if marks is not None:
+                marks[k].record()
+            k += 1
+
+        cur, cur_off = x, None
+        for s in range(self.insertions):
+            mark()
+            _lib.check("mpm_argmax", lib.mpm_argmax(_p(cur), _p(cur_off), B, N, D, dt, _p(self.nb[s]), None, st))
+            mark()
+            _lib.check("mpm_pair_compact", lib.mpm_pair_compact(_p(self.nb[s]), _p(cur_off), B, N, _p(self.map[s]),
+                                                                _p(self.src[s]), _p(self.count[s]), st))
+            mark()
+            _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(cur), _p(cur_off), _p(self.src[s]),
+                                                                _p(self.count[s]), B, N, D, dt, _p(self.y[s]),
+                                                                _p(self.y_off[s]), st))
+            cur, cur_off = self.y[s], self.y_off[s]
+        if self.insertions == 1:
+            mark()
+            self.rstar.copy_(self.map[0])
+        else:
+            mark()
+            _lib.check("mpm_compose", lib.mpm_compose(_p(self.map[0]), _p(self.map[1]), B, N, _p(self.rstar), st))
+            for s in range(2, self.insertions):
+                mark()
+                _lib.check("mpm_compose", lib.mpm_compose(_p(self.rstar), _p(self.map[s]), B, N, _p(self.rstar),
+                                                          st))
+        mark()
+        _lib.check("mpm_unmerge", lib.mpm_unmerge(_p(cur), _p(cur_off), _p(self.rstar), None, 0, B, N, D, dt,
+                                                  _p(self.out), st))
+        mark()
+        return self.out
+
+    def n_marks(self) -> int:
+        return len(self.kernel_names) + 1
