@@ -73,16 +73,18 @@ struct Mfma<F32> {
     }
 };
 
-// WC x WQ waves; each wave computes MT x NT tiles of 32 candidates x 32 queries.
-template <class S, int WC, int WQ, int MT, int NT>
+constexpr int kXcds = 8;  // MI355X: workgroups are dealt round-robin to 8 XCDs, each with its own L2
+
+// WC x WQ waves; each wave computes MT x NT tiles of 32 candidates x 32 queries;
+// CHUNK bytes of the K dimension are staged per LDS buffer.
+template <class S, int WC, int WQ, int MT, int NT, int CHUNK>
 __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
-    const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int N, int D,
-    int32_t* __restrict__ nb, float* __restrict__ best)
+    const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int qblocks,
+    int xcd_major, int32_t* __restrict__ nb, float* __restrict__ best)
 {
     constexpr int THREADS = WC * WQ * kWave;
     constexpr int CT = WC * MT * 32;     // candidates per tile
     constexpr int QT = WQ * NT * 32;     // queries per workgroup
-    constexpr int CHUNK = 128;           // bytes of the K dimension per LDS stage
     constexpr int STRIDE = CHUNK + 16;   // padded LDS row pitch (bytes)
     constexpr int VPR = CHUNK / 16;      // 16-byte vectors per row per stage
     constexpr int CLOADS = CT * VPR / THREADS;
@@ -95,8 +97,21 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
     __shared__ float red_v[WC][QT];
     __shared__ int32_t red_i[WC][QT];
 
-    const int b = blockIdx.y;
-    const int qbase = blockIdx.x * QT;
+    // Workgroup -> (image, query block). With xcd_major, consecutive ids that the
+    // hardware sends to the same XCD walk through the query blocks of one image
+    // before the next, so an image's candidate tiles are re-read from that XCD's L2.
+    int b, qb;
+    if (xcd_major) {
+        const int xcd = blockIdx.x % kXcds;
+        const int slot = blockIdx.x / kXcds;
+        b = xcd + kXcds * (slot / qblocks);
+        qb = slot % qblocks;
+    } else {
+        b = blockIdx.x / qblocks;
+        qb = blockIdx.x % qblocks;
+    }
+    if (b >= B) return;
+    const int qbase = qb * QT;
     const int row0 = x_off ? x_off[b] : b * N;
     const int n = x_off ? x_off[b + 1] - row0 : N;
     if (qbase >= n) return;  // uniform over the workgroup, before any barrier
@@ -191,18 +206,19 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
             for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt) Mfma<S>::mma(acc[mt][nt], a[mt], q[nt]);
-            if (wq == 0) {
+            // Candidate norms: m-tile mt is summed by the wave with wq == mt % WQ only.
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) ss[mt] = Mfma<S>::sumsq(a[mt], ss[mt]);
-            }
+            for (int mt = 0; mt < MT; ++mt)
+                if (mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(a[mt], ss[mt]);
         }
 
         const int tile = step / nchunks;
         const bool tile_end = (step - tile * nchunks) == nchunks - 1;
-        if (tile_end && wq == 0) {
+        if (tile_end) {
             // Lanes l and l+32 hold the two k halves of candidate row lrow.
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
+                if (mt % WQ != wq) continue;
                 const float t = ss[mt] + __shfl_xor(ss[mt], 32);
                 ss[mt] = 0.0f;
                 if (khalf == 0) inv_c[tile & 1][wc * MT * 32 + mt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
@@ -287,14 +303,17 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
     }
 }
 
-template <class S, int WC, int WQ, int MT, int NT>
+template <class S, int WC, int WQ, int MT, int NT, int CHUNK>
 hipError_t launch_t(const void* x, const int32_t* x_off, int B, int N, int D, int32_t* nb, float* best,
                     hipStream_t stream)
 {
     constexpr int QT = WQ * NT * 32;
-    dim3 grid((N + QT - 1) / QT, B);
-    hipLaunchKernelGGL((affinity_argmax_kernel<S, WC, WQ, MT, NT>), grid, dim3(WC * WQ * kWave), 0, stream,
-                       static_cast<const uint8_t*>(x), x_off, N, D, nb, best);
+    const int qblocks = (N + QT - 1) / QT;
+    const int xcd_major = B >= kXcds ? 1 : 0;
+    const long groups = xcd_major ? (long)kXcds * ((B + kXcds - 1) / kXcds) * qblocks : (long)B * qblocks;
+    hipLaunchKernelGGL((affinity_argmax_kernel<S, WC, WQ, MT, NT, CHUNK>), dim3((unsigned)groups),
+                       dim3(WC * WQ * kWave), 0, stream, static_cast<const uint8_t*>(x), x_off, B, N, D, qblocks,
+                       xcd_major, nb, best);
     return hipGetLastError();
 }
 
@@ -303,8 +322,8 @@ hipError_t launch_t(const void* x, const int32_t* x_off, int B, int N, int D, in
 hipError_t launch_argmax(const void* x, const int32_t* x_off, int B, int N, int D, int dt, int32_t* nb,
                          float* best, hipStream_t stream)
 {
-    if (dt == kBf16) return launch_t<Bf16, 2, 2, 2, 2>(x, x_off, B, N, D, nb, best, stream);
-    return launch_t<F32, 2, 2, 2, 2>(x, x_off, B, N, D, nb, best, stream);
+    if (dt == kBf16) return launch_t<Bf16, 2, 4, 4, 2, 128>(x, x_off, B, N, D, nb, best, stream);
+    return launch_t<F32, 2, 2, 2, 2, 128>(x, x_off, B, N, D, nb, best, stream);
 }
 
 }  // namespace mpm
