@@ -39,6 +39,7 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
+    """Hash of the affinity kernel's source, to tell whether stored counters still apply."""
     p = os.path.join(ROOT, "paper_2604_05718_amd", "csrc", "affinity_argmax.hip")
     return hashlib.sha256(open(p, "rb").read()).hexdigest()
 
@@ -99,7 +100,21 @@ def main() -> int:
     ap.add_argument("--workload", default="vit_b_512")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU oracle baseline (0 skips it)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only run 5 device-to-device copies of this many MiB (counter calibration) and exit")
     args = ap.parse_args()
+
+    if args.copy_calibration_mib:
+        import torch
+
+        n = args.copy_calibration_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"bench: copied {args.copy_calibration_mib} MiB 5 times")
+        return 0
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -163,7 +178,7 @@ def main() -> int:
         kernels.append(ent)
 
     # Dominant kernel: the fused affinity-argmax (both insertions' launches).
-    a_idx = [i for i, n in enumerate(names) if n.startswith("argmax")]
+    a_idx = [i for i, n in enumerate(names) if n.startswith("affinity")]
     a_flops = sum(work[i][1] for i in a_idx)
     a_ms = sum(per_kernel_ms[i] for i in a_idx)
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS

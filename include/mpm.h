@@ -38,7 +38,7 @@
  *     MPM_ERR_INVALID_ARG  null or misaligned pointer, B < 1, N < 1, D < 1,
  *                          D not a multiple of 8 (bf16) / 4 (f32), bad dtype;
  *     MPM_ERR_UNSUPPORTED  N above MPM_MAX_N, B above MPM_MAX_B, D above MPM_MAX_D;
- *     MPM_ERR_WORKSPACE    workspace smaller than mpm_merge_workspace_bytes;
+ *     MPM_ERR_WORKSPACE    workspace smaller than mpm_workspace_bytes;
  *     MPM_ERR_HIP          a launch failed; mpm_last_hip_error() holds the
  *                          hipError_t (per host thread).
  *   Device-side faults surface at the caller's next synchronisation.
@@ -82,17 +82,48 @@ const char* mpm_status_string(int status);
 int mpm_last_hip_error(void);
 
 /*
- * Nearest neighbours (Eq. 1 and the argmax of Sec. 3.2).
- *   nb[b*N + i] = argmax_{j != i, j < n_b} cos(x_i, x_j), lowest j on equal
- *                 scores; -1 when n_b == 1.
- *   best[b*N + i] (optional, may be NULL) = the float32 cosine of that pair.
- * x: rows of dtype `dt` (dense or packed by x_off). Entries i >= n_b are not
- * written. Scores are (x_i . x_j) / max(||x_j||, 1e-12) with the dot product
- * accumulated in float32 from the stored values (bf16 products are exact in
- * float32); the affinity matrix is never written to memory.
+ * Device workspace shared by mpm_affinity, mpm_argmax, mpm_pair_compact_ws and
+ * mpm_merge: bytes needed for a batch of B images of at most N tokens. The
+ * caller allocates it (256-byte aligned) and owns it; consecutive calls on one
+ * stream may reuse it. Layout, as byte offsets returned by
+ * mpm_workspace_offsets (each 256-byte aligned):
+ *   nb    int32[B*N]          nearest neighbour per token (slot layout);
+ *   src   int32[2*B*N]        (representative, partner) per cluster;
+ *   count int32[B]            clusters per image;
+ *   pv    float[B*T*N], pi int32[B*T*N]  per-candidate-tile argmax partials,
+ *                             T = ceil(N / 256).
+ * Returns 0 for B < 1 or N < 1.
  */
-int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt,
-               int32_t* nb, float* best, void* stream);
+size_t mpm_workspace_bytes(int32_t B, int32_t N);
+
+/* Byte offsets of the workspace regions listed above; any pointer may be NULL.
+ * Returns MPM_OK, or MPM_ERR_INVALID_ARG for B < 1 or N < 1. */
+int mpm_workspace_offsets(int32_t B, int32_t N, size_t* nb, size_t* src, size_t* count, size_t* pv,
+                          size_t* pi);
+
+/*
+ * Cosine affinity and its self-masked row argmax, per candidate tile (Eq. 1
+ * and the argmax of Sec. 3.2), into the workspace partials: for every query i
+ * and candidate tile t, the best score (x_i . x_j) / max(||x_j||, 1e-12) over
+ * the tile's candidates j != i, j < n_b, and that j (lowest j among equal
+ * scores). The dot products are accumulated in float32 on MFMA from the
+ * stored values (bfloat16 products are exact in float32); the N x N affinity
+ * is never written to memory. Dividing by ||x_i|| too would not move the
+ * argmax of row i, so it is not applied.
+ * x: rows of dtype `dt`, dense or packed by x_off.
+ */
+int mpm_affinity(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* ws,
+                 size_t ws_bytes, void* stream);
+
+/*
+ * Nearest neighbours: mpm_affinity, then the reduction of the partials.
+ *   nb[b*N + i] = argmax_{j != i, j < n_b} cos(x_i, x_j), lowest j on equal
+ *                 scores; -1 when n_b == 1. Entries i >= n_b are not written.
+ *   best[b*N + i] (optional, may be NULL) = the float32 cosine of that pair.
+ * nb and best are caller arrays (not the workspace).
+ */
+int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* nb,
+               float* best, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Mutual pairs and compact ids (Sec. 3.2, Alg. 1) from nb.
@@ -106,29 +137,33 @@ int mpm_pair_compact(const int32_t* nb, const int32_t* x_off, int32_t B, int32_t
                      int32_t* map, int32_t* src, int32_t* count, void* stream);
 
 /*
+ * mpm_pair_compact reading the partials mpm_affinity left in the workspace
+ * (D and dt must be those of that call): reduces them to nb (written to the
+ * workspace's nb region), then writes map, and src/count into the workspace.
+ */
+int mpm_pair_compact_ws(const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* map,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Cluster means (Eq. 2), packed.
  *   y_off[0] = 0, y_off[b+1] = y_off[b] + count[b];
- *   y[y_off[b] + k] = mean of the rows src pairs name for cluster k of image b,
+ *   y[y_off[b] + k] = mean of the rows src names for cluster k of image b,
  *     computed in float32 and rounded once (nearest even) to `dt`; a
  *     singleton is copied bit for bit.
- * y has room for sum_b count[b] rows (at most B*N). x as in mpm_argmax.
+ * y has room for sum_b count[b] rows (at most B*N). x as in mpm_affinity.
  */
 int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count,
                      int32_t B, int32_t N, int32_t D, int32_t dt,
                      void* y, int32_t* y_off, void* stream);
 
-/* Bytes of device workspace mpm_merge needs (nb, src, count; 256-byte aligned). */
-size_t mpm_merge_workspace_bytes(int32_t B, int32_t N);
-
 /*
- * One MPM insertion (Alg. 1) = mpm_argmax, mpm_pair_compact and
- * mpm_pair_average in order on `stream`.
+ * One MPM insertion (Alg. 1) = mpm_affinity, mpm_pair_compact_ws and
+ * mpm_pair_average (src and count from the workspace) in order on `stream`.
  *   x, x_off: input tokens (dense or packed);
  *   y, y_off: merged tokens, packed (capacity B*N rows), offsets int32[B+1];
  *   map: int32[B*N] merge map in slot layout (-1 beyond n_b);
- *   ws: device workspace of at least mpm_merge_workspace_bytes(B, N) bytes,
- *       256-byte aligned. Its layout: nb int32[B*N] at offset 0 (readable
- *       after the call), then src and count.
+ *   ws: workspace of at least mpm_workspace_bytes(B, N) bytes; nb, src and
+ *       count are readable there after the call.
  * Feed (y, y_off) as (x, x_off) of the next insertion.
  */
 int mpm_merge(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt,

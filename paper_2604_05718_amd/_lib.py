@@ -25,15 +25,20 @@ _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
 _sz = ctypes.c_size_t
 
+_szp = ctypes.POINTER(ctypes.c_size_t)
+
 # name -> (restype, argtypes); mirrors include/mpm.h
 SIGNATURES = {
     "mpm_version": (ctypes.c_char_p, []),
     "mpm_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "mpm_last_hip_error": (ctypes.c_int, []),
-    "mpm_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp]),
+    "mpm_workspace_bytes": (_sz, [_i32, _i32]),
+    "mpm_workspace_offsets": (ctypes.c_int, [_i32, _i32, _szp, _szp, _szp, _szp, _szp]),
+    "mpm_affinity": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp]),
+    "mpm_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "mpm_pair_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "mpm_pair_compact_ws": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
     "mpm_pair_average": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp]),
-    "mpm_merge_workspace_bytes": (_sz, [_i32, _i32]),
     "mpm_merge": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
     "mpm_compose": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp, _vp]),
     "mpm_unmerge": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
@@ -84,6 +89,13 @@ def load():
         fn.argtypes = args
     _lib = lib
     return lib
+
+
+def workspace_offsets(B: int, N: int) -> dict:
+    """Byte offsets of the workspace regions (nb, src, count, pv, pi)."""
+    vals = [ctypes.c_size_t() for _ in range(5)]
+    check("mpm_workspace_offsets", load().mpm_workspace_offsets(B, N, *[ctypes.byref(v) for v in vals]))
+    return dict(zip(("nb", "src", "count", "pv", "pi"), (v.value for v in vals)))
 
 
 def check(fn: str, status: int) -> None:

@@ -56,13 +56,22 @@ def _rows(x: torch.Tensor, N: int | None, x_off: torch.Tensor | None):
     return x, x_off.numel() - 1, int(N), x.shape[1]
 
 
-def argmax(x, x_off=None, N=None, with_best=False):
+def _workspace(B, N, device, ws=None):
+    need = workspace_bytes(B, N)
+    if ws is None or ws.numel() < need:
+        ws = torch.empty((need,), dtype=torch.uint8, device=device)
+    return ws
+
+
+def argmax(x, x_off=None, N=None, with_best=False, ws=None):
     """nb [B, N] int32 (and best [B, N] float32 cosines when ``with_best``)."""
     x2, B, N, D = _rows(x, N, x_off)
     nb = torch.empty((B, N), dtype=torch.int32, device=x.device)
     best = torch.empty((B, N), dtype=torch.float32, device=x.device) if with_best else None
+    ws = _workspace(B, N, x.device, ws)
     lib = _lib.load()
-    _lib.check("mpm_argmax", lib.mpm_argmax(_p(x2), _p(x_off), B, N, D, _dt(x), _p(nb), _p(best), _stream()))
+    _lib.check("mpm_argmax", lib.mpm_argmax(_p(x2), _p(x_off), B, N, D, _dt(x), _p(nb), _p(best), _p(ws),
+                                            ws.numel(), _stream()))
     return (nb, best) if with_best else nb
 
 
@@ -91,7 +100,7 @@ def pair_average(x, src, count, x_off=None, N=None):
 
 
 def workspace_bytes(B: int, N: int) -> int:
-    return int(_lib.load().mpm_merge_workspace_bytes(B, N))
+    return int(_lib.load().mpm_workspace_bytes(B, N))
 
 
 @dataclass
@@ -112,9 +121,7 @@ def merge(x, x_off=None, N=None, ws=None) -> Merged:
     """One MPM insertion (Alg. 1)."""
     x2, B, N, D = _rows(x, N, x_off)
     dev = x.device
-    need = workspace_bytes(B, N)
-    if ws is None or ws.numel() < need:
-        ws = torch.empty((need,), dtype=torch.uint8, device=dev)
+    ws = _workspace(B, N, dev, ws)
     y = torch.empty((B * N, D), dtype=x.dtype, device=dev)
     y_off = torch.empty((B + 1,), dtype=torch.int32, device=dev)
     m = torch.empty((B, N), dtype=torch.int32, device=dev)
@@ -176,7 +183,9 @@ class Schedule:
     """Preallocated MPM schedule for a fixed batch shape: every buffer is
     allocated once, so ``run`` only launches kernels (no allocation, no host
     synchronisation). Stage s consumes stage s-1's packed output (Sec. 3.3);
-    the composed map and the reconstruction follow (Eq. 3, Eq. 4).
+    the composed map and the reconstruction follow (Eq. 3, Eq. 4). Each
+    insertion runs the three kernels of ``mpm_merge`` through its step entry
+    points (affinity, compaction, average), so they can be timed one by one.
 
     ``run(x, marks=None)``: when ``marks`` is a list of ``n_marks()``
     torch.cuda.Event objects, event k is recorded on the current stream just
@@ -189,9 +198,12 @@ class Schedule:
         self.B, self.N, self.D, self.dtype, self.insertions = B, N, D, dtype, insertions
         dev = torch.device(device)
         i32 = dict(dtype=torch.int32, device=dev)
-        self.nb = [torch.empty((B, N), **i32) for _ in range(insertions)]
-        self.src = [torch.empty((B, N, 2), **i32) for _ in range(insertions)]
-        self.count = [torch.empty((B,), **i32) for _ in range(insertions)]
+        nbytes = workspace_bytes(B, N)
+        off = _lib.workspace_offsets(B, N)
+        self.ws = [torch.empty((nbytes,), dtype=torch.uint8, device=dev) for _ in range(insertions)]
+        self.nb = [w[off["nb"]:off["nb"] + 4 * B * N].view(torch.int32).view(B, N) for w in self.ws]
+        self.src = [w[off["src"]:off["src"] + 8 * B * N].view(torch.int32).view(B, N, 2) for w in self.ws]
+        self.count = [w[off["count"]:off["count"] + 4 * B].view(torch.int32) for w in self.ws]
         self.map = [torch.empty((B, N), **i32) for _ in range(insertions)]
         self.y = [torch.empty((B * N, D), dtype=dtype, device=dev) for _ in range(insertions)]
         self.y_off = [torch.empty((B + 1,), **i32) for _ in range(insertions)]
@@ -204,11 +216,15 @@ class Schedule:
     def kernel_names(self) -> list:
         names = []
         for s in range(self.insertions):
-            names += [f"argmax{s + 1}", f"compact{s + 1}", f"average{s + 1}"]
-        names += ["compose"] * max(0, self.insertions - 1) + ["unmerge"]
+            names += [f"affinity{s + 1}", f"compact{s + 1}", f"average{s + 1}"]
         if self.insertions == 1:
-            names.insert(len(names) - 1, "copy_map")
-        return names
+            names += ["copy_map"]
+        else:
+            names += ["compose"] * (self.insertions - 1)
+        return names + ["unmerge"]
+
+    def n_marks(self) -> int:
+        return len(self.kernel_names) + 1
 
     def run(self, x: torch.Tensor, marks=None) -> torch.Tensor:
         if x.shape != (self.B, self.N, self.D) or x.dtype != self.dtype or not x.is_contiguous():
@@ -224,11 +240,12 @@ class Schedule:
 
         cur, cur_off = x, None
         for s in range(self.insertions):
+            ws = self.ws[s]
             mark()
-            _lib.check("mpm_argmax", lib.mpm_argmax(_p(cur), _p(cur_off), B, N, D, dt, _p(self.nb[s]), None, st))
+            _lib.check("mpm_affinity", lib.mpm_affinity(_p(cur), _p(cur_off), B, N, D, dt, _p(ws), ws.numel(), st))
             mark()
-            _lib.check("mpm_pair_compact", lib.mpm_pair_compact(_p(self.nb[s]), _p(cur_off), B, N, _p(self.map[s]),
-                                                                _p(self.src[s]), _p(self.count[s]), st))
+            _lib.check("mpm_pair_compact_ws", lib.mpm_pair_compact_ws(_p(cur_off), B, N, D, dt, _p(self.map[s]),
+                                                                      _p(ws), ws.numel(), st))
             mark()
             _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(cur), _p(cur_off), _p(self.src[s]),
                                                                 _p(self.count[s]), B, N, D, dt, _p(self.y[s]),
@@ -249,6 +266,3 @@ class Schedule:
                                                   _p(self.out), st))
         mark()
         return self.out
-
-    def n_marks(self) -> int:
-        return len(self.kernel_names) + 1

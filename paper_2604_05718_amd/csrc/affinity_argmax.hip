@@ -75,12 +75,23 @@ struct Mfma<F32> {
 
 constexpr int kXcds = 8;  // MI355X: workgroups are dealt round-robin to 8 XCDs, each with its own L2
 
+// Workgroup barrier that waits only for this wave's LDS operations (not for
+// outstanding global loads, which keep streaming into other LDS buffers).
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt unconstrained
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Register-staged variant (any 16-byte row size, float32 or bfloat16): a
+// workgroup owns QT queries and loops over every candidate tile itself.
 // WC x WQ waves; each wave computes MT x NT tiles of 32 candidates x 32 queries;
 // CHUNK bytes of the K dimension are staged per LDS buffer.
 template <class S, int WC, int WQ, int MT, int NT, int CHUNK>
 __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int qblocks,
-    int xcd_major, int32_t* __restrict__ nb, float* __restrict__ best)
+    int xcd_major, int T, float* __restrict__ pv, int32_t* __restrict__ pi)
 {
     constexpr int THREADS = WC * WQ * kWave;
     constexpr int CT = WC * MT * 32;     // candidates per tile
@@ -292,20 +303,381 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
                 i = oi;
             }
         }
-        nb[(long)b * N + qi] = i;
-        if (best) {
-            // Diagnostic only: divide by the query's own norm to report the cosine.
-            const uint8_t* xr = ximg + qi * rowbytes;
-            float t = 0.0f;
-            for (long kk = 0; kk < rowbytes; kk += 16) t = Mfma<S>::sumsq(load16(xr + kk), t);
-            best[(long)b * N + qi] = i >= 0 ? v / fmaxf(sqrtf(t), 1e-12f) : -__builtin_inff();
-        }
+        // This kernel covers every candidate itself: one partial, in tile slot 0.
+        pv[(long)b * T * N + qi] = v;
+        pi[(long)b * T * N + qi] = i;
     }
 }
 
+// Persistent variant for bfloat16 rows that are a whole number of CB-byte
+// chunks. Work item = (image, query block of QT, candidate tile of CT); an item
+// streams its two operand blocks through a STAGES-deep ring of LDS buffers
+// filled by direct global->LDS loads (global_load_lds_dwordx4), runs the K loop
+// on MFMA, then reduces its tile to one (score, index) partial per query.
+//
+// Scheduling for the 8 per-XCD L2 caches: workgroups are dealt round-robin to
+// the XCDs, so workgroup w serves XCD group w % xcds; a group owns the images
+// b = group + xcds * i and its `slots` workgroups take the group's items in
+// order (item k goes to slot k % slots). All items of an image therefore run at
+// the same time on one XCD, in lockstep over K, and each 256-row block is
+// fetched from HBM once and re-read from that XCD's L2 by the other items that
+// use it, instead of being refetched once per candidate tile.
+//
+// LDS layout of one stage: CB = 128 bytes of K per row, rows of an operand
+// stored one after the other (128 B each), with the eight 16-byte columns of a
+// row permuted by an XOR swizzle: column c of row r sits in slot
+// c ^ swz(r), swz(r) = ((r % 8) / 2) | (((r / 8) % 2) << 2). One load instruction
+// fills 8 consecutive rows: lane l reads 16 bytes of row l/8 (8 lanes cover
+// one full 128-byte line of global memory) and lands at 16*l of a contiguous
+// 1 KB. An MFMA fragment read (rows r..r+31 of one 16-byte column per lane
+// half) then touches 16 distinct 16-byte bank groups in every 16-lane group,
+// so it is free of bank conflicts on the 64-bank LDS.
+// Rows past the image are clamped to its last row (their scores are masked).
+template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES>
+__global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
+    const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int T, int xcds,
+    int slots, float* __restrict__ pv, int32_t* __restrict__ pi)
+{
+    constexpr int THREADS = WC * WQ * kWave;
+    constexpr int WAVES = WC * WQ;
+    constexpr int CT = WC * MT * 32;
+    constexpr int QT = WQ * NT * 32;
+    static_assert(CB == 128, "the swizzled layout assumes 128-byte row chunks");
+    constexpr int LOADS = (CT + QT) / 8 / WAVES;      // load instructions (8 rows each) per wave per stage
+    constexpr int STAGE_BYTES = (CT + QT) * CB;
+    static_assert((CT + QT) / 8 % WAVES == 0, "stage/wave mismatch");
+    static_assert((STAGES - 2) * LOADS < 64, "vmcnt range");
+    static_assert(STAGES >= 2 && STAGES <= 5, "pipeline depth");
+
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[STAGES * STAGE_BYTES];
+    __shared__ __attribute__((aligned(16))) float inv_c[2][CT];
+    __shared__ float red_v[WC][QT];
+    __shared__ int32_t red_i[WC][QT];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int wave = tid / kWave;
+    const int wc = wave % WC;
+    const int wq = wave / WC;
+    const int lrow = lane & 31;
+    const int khalf = lane >> 5;
+
+    const int group = blockIdx.x % xcds;
+    const int slot = blockIdx.x / xcds;
+    const int per_img = ((N + QT - 1) / QT) * T;
+    const int nimg = (B - group + xcds - 1) / xcds;
+    const int nitems = nimg * per_img;
+    const long rowbytes = (long)D * S::kBytes;
+    const int nchunks = (int)(rowbytes / CB);
+
+    // Item cursor; all fields are uniform over the workgroup.
+    struct Item {
+        int k, b, qbase, cbase, n, row0;
+    };
+    auto find = [&](int k) {
+        Item it;
+        for (; k < nitems; k += slots) {
+            const int ib = k / per_img;
+            const int w = k - ib * per_img;
+            const int b = group + xcds * ib;
+            const int qb = w / T;
+            const int t = w - qb * T;
+            const int row0 = x_off ? x_off[b] : b * N;
+            const int n = x_off ? x_off[b + 1] - row0 : N;
+            if (qb * QT < n && t * CT < n) {
+                it.k = k; it.b = b; it.qbase = qb * QT; it.cbase = t * CT; it.n = n; it.row0 = row0;
+                return it;
+            }
+        }
+        it.k = nitems; it.b = 0; it.qbase = 0; it.cbase = 0; it.n = 1; it.row0 = 0;
+        return it;
+    };
+
+    // Swizzle of the 16-byte column slot for a row (see the layout note above).
+    auto swz = [](int r) { return ((r & 7) >> 1) | (((r >> 3) & 1) << 2); };
+    const int lrow8 = lane >> 3;                          // row inside an 8-row load group
+    const int lslot = lane & 7;                           // column slot this lane fills
+    // Each wave fills 8 * LOADS consecutive rows of one operand block; row r of
+    // a load group i has r % 8 == lrow8 and (r / 8) % 2 == i % 2, so its slot
+    // swizzle is one of two per-lane constants.
+    static_assert(CT % (8 * LOADS) == 0, "a wave's rows must not straddle the two operands");
+    const int wrow0 = wave * 8 * LOADS;                   // first row of this wave in [cand; query]
+    const bool w_is_q = wrow0 >= CT;
+    const int wr0 = w_is_q ? wrow0 - CT : wrow0;          // first row inside its operand block
+    const uint32_t col_even = (uint32_t)((lslot ^ (lrow8 >> 1)) << 4);
+    const uint32_t col_odd = (uint32_t)((lslot ^ (lrow8 >> 1) ^ 4) << 4);
+    // Byte offsets (from the image's first row) of this lane's 16-byte pieces for
+    // the issue cursor's item; they change per item, not per chunk.
+    struct Offsets {
+        uint32_t v[LOADS];
+    };
+    auto offsets_of = [&](const Item& it) {
+        Offsets o;
+        const int first = (w_is_q ? it.qbase : it.cbase) + wr0 + lrow8;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            int row = first + i * 8;
+            row = row < it.n ? row : it.n - 1;
+            o.v[i] = (uint32_t)row * (uint32_t)rowbytes + ((i & 1) ? col_odd : col_even);
+        }
+        return o;
+    };
+    auto issue = [&](const Item& it, const Offsets& o, int chunk, int buf) {
+        uint8_t* l0 = lds + buf * STAGE_BYTES + wrow0 * CB;
+        const uint8_t* base = x + (long)it.row0 * rowbytes + (long)chunk * CB;   // uniform
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) {
+            const uint32_t off = o.v[i];  // a non-dependent operand type keeps the host stub instantiable
+            __builtin_amdgcn_global_load_lds(base + off, (__attribute__((address_space(3))) void*)(l0 + i * 8 * CB), 16,
+                                             0, 0);
+        }
+    };
+
+    f32x16 acc[MT][NT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x16{};
+    float ss[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) ss[mt] = 0.0f;
+
+    Item ii = find(slot);  // issue cursor
+    Offsets ioff = offsets_of(ii);
+    int ichunk = 0;
+    int issued = 0;
+    auto issue_next = [&]() {
+        if (ii.k >= nitems) return;
+        issue(ii, ioff, ichunk, issued % STAGES);
+        ++issued;
+        if (++ichunk == nchunks) {
+            ichunk = 0;
+            ii = find(ii.k + slots);
+            if (ii.k < nitems) ioff = offsets_of(ii);
+        }
+    };
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s) issue_next();
+
+    Item ci = find(slot);  // compute cursor
+    int cchunk = 0;
+    int consumed = 0;
+    int items_done = 0;
+    while (ci.k < nitems) {
+        // Stages issued after the one consumed now may stay in flight.
+        const int pending = issued - consumed - 1;
+        if (pending >= STAGES - 2) __builtin_amdgcn_s_waitcnt(0x0F70 | (((STAGES - 2) * LOADS) & 15) | ((((STAGES - 2) * LOADS) >> 4) << 14));
+        else if (STAGES > 3 && pending == 2) __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * LOADS) & 15) | (((2 * LOADS) >> 4) << 14));
+        else if (STAGES > 2 && pending == 1) __builtin_amdgcn_s_waitcnt(0x0F70 | (LOADS & 15) | ((LOADS >> 4) << 14));
+        else __builtin_amdgcn_s_waitcnt(0x0F70);
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        issue_next();  // refills the buffer every wave finished reading last step
+
+        const uint8_t* sbase = lds + (consumed % STAGES) * STAGE_BYTES;
+        // Row lrow of every 32-row fragment has the same swizzle (32 is a multiple of 16).
+        const uint8_t* lc = sbase + (wc * MT * 32 + lrow) * CB;
+        const uint8_t* lq = sbase + (CT + wq * NT * 32 + lrow) * CB;
+        const int sw = swz(lrow);
+#pragma unroll
+        for (int g = 0; g < CB / 32; ++g) {
+            const int col = ((2 * g + khalf) ^ sw) << 4;
+            u32x4 a[MT], q[NT];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) a[mt] = *reinterpret_cast<const u32x4*>(lc + mt * 32 * CB + col);
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) q[nt] = *reinterpret_cast<const u32x4*>(lq + nt * 32 * CB + col);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) Mfma<S>::mma(acc[mt][nt], a[mt], q[nt]);
+            // Candidate norms: m-tile mt is summed by the wave with wq == mt % WQ only.
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                if (mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(a[mt], ss[mt]);
+        }
+        ++consumed;
+        if (++cchunk < nchunks) continue;
+
+        // ---- end of an item: norms, scores, per-query partial argmax ----
+        const int par = items_done & 1;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            if (mt % WQ != wq) continue;
+            const float t = ss[mt] + __shfl_xor(ss[mt], 32);  // lanes l, l+32: the two k halves
+            ss[mt] = 0.0f;
+            if (khalf == 0) inv_c[par][wc * MT * 32 + mt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+        }
+        lds_barrier();
+        const float* iv = inv_c[par];
+        const int n = ci.n;
+        const int cb = ci.cbase;
+        const bool need_mask = (cb + CT > n) || (cb < ci.qbase + QT && ci.qbase < cb + CT);
+        // Accumulator element r = 4g+e of this lane is candidate row 8g + 4*khalf + e of
+        // its 32-row tile, so rows ascend with r. Each 16-value group is reduced by a
+        // tournament in which the left (lower) entry wins ties, then merged into the
+        // running best in ascending tile order with a strict >: the lowest index
+        // wins among equal scores, as in a left-to-right scan.
+        float bv[NT];
+        int32_t bi[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            const int qi = ci.qbase + wq * NT * 32 + nt * 32 + lrow;
+            float vb = -__builtin_inff();
+            int32_t jb = -1;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const int jt = cb + wc * MT * 32 + mt * 32 + 4 * khalf;  // candidate of r = 0
+                float sc[16];
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const f32x4 ivv = *reinterpret_cast<const f32x4*>(&iv[wc * MT * 32 + mt * 32 + 8 * g + 4 * khalf]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) sc[4 * g + e] = acc[mt][nt][4 * g + e] * ivv[e];
+                }
+                if (need_mask) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int j = jt + 8 * (r >> 2) + (r & 3);
+                        sc[r] = (j < n && j != qi) ? sc[r] : -__builtin_inff();
+                    }
+                }
+                float v8[8];
+                int r8[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const bool c = sc[2 * k + 1] > sc[2 * k];
+                    v8[k] = c ? sc[2 * k + 1] : sc[2 * k];
+                    r8[k] = c ? 2 * k + 1 : 2 * k;
+                }
+                float v4[4];
+                int r4[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const bool c = v8[2 * k + 1] > v8[2 * k];
+                    v4[k] = c ? v8[2 * k + 1] : v8[2 * k];
+                    r4[k] = c ? r8[2 * k + 1] : r8[2 * k];
+                }
+                const bool c0 = v4[1] > v4[0];
+                const float v20 = c0 ? v4[1] : v4[0];
+                const int r20 = c0 ? r4[1] : r4[0];
+                const bool c1 = v4[3] > v4[2];
+                const float v21 = c1 ? v4[3] : v4[2];
+                const int r21 = c1 ? r4[3] : r4[2];
+                const bool cf = v21 > v20;
+                const float v1 = cf ? v21 : v20;
+                const int r1 = cf ? r21 : r20;
+                const bool up = v1 > vb;
+                vb = up ? v1 : vb;
+                jb = up ? jt + r1 + 4 * (r1 >> 2) : jb;  // row 8*(r/4) + r%4 of the tile
+            }
+            bv[nt] = vb;
+            bi[nt] = jb;
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x16{};
+        // Merge the two lane halves, then the WC candidate waves (larger score, then smaller index).
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            float v = bv[nt];
+            int32_t i = bi[nt];
+            const float ov = __shfl_xor(v, 32);
+            const int32_t oi = __shfl_xor(i, 32);
+            if (ov > v || (ov == v && (uint32_t)oi < (uint32_t)i)) {
+                v = ov;
+                i = oi;
+            }
+            if (khalf == 0) {
+                const int ql = wq * NT * 32 + nt * 32 + lrow;
+                red_v[wc][ql] = v;
+                red_i[wc][ql] = i;
+            }
+        }
+        lds_barrier();
+        const int t = cb / CT;
+        for (int ql = tid; ql < QT; ql += THREADS) {
+            const int qi = ci.qbase + ql;
+            if (qi >= n) continue;
+            float v = red_v[0][ql];
+            int32_t i = red_i[0][ql];
+#pragma unroll
+            for (int w = 1; w < WC; ++w) {
+                const float ov = red_v[w][ql];
+                const int32_t oi = red_i[w][ql];
+                if (ov > v || (ov == v && (uint32_t)oi < (uint32_t)i)) {
+                    v = ov;
+                    i = oi;
+                }
+            }
+            const long o = ((long)ci.b * T + t) * N + qi;
+            pv[o] = v;
+            pi[o] = i;
+        }
+        ++items_done;
+        cchunk = 0;
+        ci = find(ci.k + slots);
+    }
+}
+
+// nb[b*N + i] = lexicographic max over the candidate-tile partials of row i
+// (larger score, then smaller index); optional cosine of the chosen pair.
+template <class S>
+__global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __restrict__ pv,
+                                                               const int32_t* __restrict__ pi,
+                                                               const uint8_t* __restrict__ x,
+                                                               const int32_t* __restrict__ x_off, int B, int N,
+                                                               int D, int T, int ct, int32_t* __restrict__ nb,
+                                                               float* __restrict__ best)
+{
+    const long g = (long)blockIdx.x * 256 + threadIdx.x;
+    if (g >= (long)B * N) return;
+    const int b = (int)(g / N);
+    const int i = (int)(g - (long)b * N);
+    const int row0 = x_off ? x_off[b] : b * N;
+    const int n = x_off ? x_off[b + 1] - row0 : N;
+    if (i >= n) return;
+    const int tiles = (n + ct - 1) / ct;
+    float v = -__builtin_inff();
+    int32_t j = -1;
+    for (int t = 0; t < tiles; ++t) {
+        const long o = ((long)b * T + t) * N + i;
+        const float ov = pv[o];
+        const int32_t oi = pi[o];
+        if (ov > v || (ov == v && (uint32_t)oi < (uint32_t)j)) {
+            v = ov;
+            j = oi;
+        }
+    }
+    nb[g] = j;
+    if (best) {
+        // Diagnostic only: divide by the query's own norm to report the cosine.
+        const long rowbytes = (long)D * S::kBytes;
+        const uint8_t* xr = x + ((long)row0 + i) * rowbytes;
+        float t2 = 0.0f;
+        for (long kk = 0; kk < rowbytes; kk += 16) t2 = Mfma<S>::sumsq(load16(xr + kk), t2);
+        best[g] = j >= 0 ? v / fmaxf(sqrtf(t2), 1e-12f) : -__builtin_inff();
+    }
+}
+
+// Persistent-kernel tile shape (bfloat16): 256 candidates x 256 queries on 8 waves.
+constexpr int kPWC = 2, kPWQ = 4, kPMT = 4, kPNT = 2, kPCB = 128, kPSTAGES = 2;
+constexpr int kPCT = kPWC * kPMT * 32;
+
+bool use_persistent(int D, int dt) { return dt == kBf16 && (2L * D) % kPCB == 0; }
+
+int device_cus()
+{
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    return cus;
+}
+
 template <class S, int WC, int WQ, int MT, int NT, int CHUNK>
-hipError_t launch_t(const void* x, const int32_t* x_off, int B, int N, int D, int32_t* nb, float* best,
-                    hipStream_t stream)
+hipError_t launch_staged(const void* x, const int32_t* x_off, int B, int N, int D, int T, float* pv, int32_t* pi,
+                         hipStream_t stream)
 {
     constexpr int QT = WQ * NT * 32;
     const int qblocks = (N + QT - 1) / QT;
@@ -313,17 +685,51 @@ hipError_t launch_t(const void* x, const int32_t* x_off, int B, int N, int D, in
     const long groups = xcd_major ? (long)kXcds * ((B + kXcds - 1) / kXcds) * qblocks : (long)B * qblocks;
     hipLaunchKernelGGL((affinity_argmax_kernel<S, WC, WQ, MT, NT, CHUNK>), dim3((unsigned)groups),
                        dim3(WC * WQ * kWave), 0, stream, static_cast<const uint8_t*>(x), x_off, B, N, D, qblocks,
-                       xcd_major, nb, best);
+                       xcd_major, T, pv, pi);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_argmax(const void* x, const int32_t* x_off, int B, int N, int D, int dt, int32_t* nb,
-                         float* best, hipStream_t stream)
+int partial_tiles(int N) { return (N + kPCT - 1) / kPCT; }
+
+int partial_tile_width(int D, int dt, int N) { return use_persistent(D, dt) ? kPCT : N; }
+
+hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, int D, int dt, float* pv, int32_t* pi,
+                           hipStream_t stream)
 {
-    if (dt == kBf16) return launch_t<Bf16, 2, 4, 4, 2, 128>(x, x_off, B, N, D, nb, best, stream);
-    return launch_t<F32, 2, 2, 2, 2, 128>(x, x_off, B, N, D, nb, best, stream);
+    const int T = partial_tiles(N);
+    if (use_persistent(D, dt)) {
+        const int cus = device_cus();
+        if (cus <= 0) return hipErrorInvalidDevice;
+        // One workgroup per CU (the stage ring fills most of the LDS). With a
+        // batch of at least 8 images, group the workgroups by XCD.
+        const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
+        const int slots = cus / xcds;
+        hipLaunchKernelGGL((affinity_partial_kernel<Bf16, kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES>), dim3(cus),
+                           dim3(kPWC * kPWQ * kWave), 0, stream, static_cast<const uint8_t*>(x), x_off, B, N, D, T,
+                           xcds, slots, pv, pi);
+        return hipGetLastError();
+    }
+    if (dt == kBf16) return launch_staged<Bf16, 2, 4, 4, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream);
+    return launch_staged<F32, 2, 2, 2, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream);
+}
+
+hipError_t launch_reduce_partials(const float* pv, const int32_t* pi, const void* x, const int32_t* x_off, int B,
+                                  int N, int D, int dt, int32_t* nb, float* best, hipStream_t stream)
+{
+    const int T = partial_tiles(N);
+    const int ct = partial_tile_width(D, dt, N);
+    const long total = (long)B * N;
+    const dim3 grid((unsigned)((total + 255) / 256));
+    const uint8_t* xp = static_cast<const uint8_t*>(x);
+    if (dt == kBf16)
+        hipLaunchKernelGGL(reduce_partials_kernel<Bf16>, grid, dim3(256), 0, stream, pv, pi, xp, x_off, B, N, D, T, ct,
+                           nb, best);
+    else
+        hipLaunchKernelGGL(reduce_partials_kernel<F32>, grid, dim3(256), 0, stream, pv, pi, xp, x_off, B, N, D, T, ct,
+                           nb, best);
+    return hipGetLastError();
 }
 
 }  // namespace mpm

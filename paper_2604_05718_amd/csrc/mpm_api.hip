@@ -45,25 +45,45 @@ bool ok_opt_int_ptr(const void* p) { return p == nullptr || aligned(p, 4); }
 constexpr size_t kAlign = 256;
 size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
-struct MergeWorkspace {
+struct Workspace {
     int32_t* nb;
     int32_t* src;
     int32_t* count;
+    float* pv;
+    int32_t* pi;
 };
 
-size_t workspace_bytes(int32_t B, int32_t N, MergeWorkspace* ws, void* base)
+struct Offsets {
+    size_t nb, src, count, pv, pi, total;
+};
+
+Offsets workspace_offsets(int32_t B, int32_t N)
 {
     const size_t slots = (size_t)B * (size_t)N;
-    const size_t nb_bytes = round_up(slots * sizeof(int32_t));
-    const size_t src_bytes = round_up(2 * slots * sizeof(int32_t));
-    const size_t cnt_bytes = round_up((size_t)B * sizeof(int32_t));
-    if (ws) {
-        char* p = static_cast<char*>(base);
-        ws->nb = reinterpret_cast<int32_t*>(p);
-        ws->src = reinterpret_cast<int32_t*>(p + nb_bytes);
-        ws->count = reinterpret_cast<int32_t*>(p + nb_bytes + src_bytes);
-    }
-    return nb_bytes + src_bytes + cnt_bytes;
+    const size_t partial = slots * (size_t)mpm::partial_tiles(N);
+    Offsets o;
+    o.nb = 0;
+    o.src = o.nb + round_up(slots * sizeof(int32_t));
+    o.count = o.src + round_up(2 * slots * sizeof(int32_t));
+    o.pv = o.count + round_up((size_t)B * sizeof(int32_t));
+    o.pi = o.pv + round_up(partial * sizeof(float));
+    o.total = o.pi + round_up(partial * sizeof(int32_t));
+    return o;
+}
+
+// Checks and carves the workspace; returns MPM_OK or an error status.
+int carve(void* ws, size_t ws_bytes, int32_t B, int32_t N, Workspace* w)
+{
+    if (ws == nullptr || !aligned(ws, kAlign)) return MPM_ERR_INVALID_ARG;
+    const Offsets o = workspace_offsets(B, N);
+    if (ws_bytes < o.total) return MPM_ERR_WORKSPACE;
+    char* p = static_cast<char*>(ws);
+    w->nb = reinterpret_cast<int32_t*>(p + o.nb);
+    w->src = reinterpret_cast<int32_t*>(p + o.src);
+    w->count = reinterpret_cast<int32_t*>(p + o.count);
+    w->pv = reinterpret_cast<float*>(p + o.pv);
+    w->pi = reinterpret_cast<int32_t*>(p + o.pi);
+    return MPM_OK;
 }
 
 hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
@@ -88,14 +108,48 @@ const char* mpm_status_string(int status)
 
 int mpm_last_hip_error(void) { return g_last_hip_error; }
 
-int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* nb,
-               float* best, void* stream)
+size_t mpm_workspace_bytes(int32_t B, int32_t N)
 {
-    const int s = check_rows(B, N, D, dt);
+    if (B < 1 || N < 1) return 0;
+    return workspace_offsets(B, N).total;
+}
+
+int mpm_workspace_offsets(int32_t B, int32_t N, size_t* nb, size_t* src, size_t* count, size_t* pv, size_t* pi)
+{
+    if (B < 1 || N < 1) return MPM_ERR_INVALID_ARG;
+    const Offsets o = workspace_offsets(B, N);
+    if (nb) *nb = o.nb;
+    if (src) *src = o.src;
+    if (count) *count = o.count;
+    if (pv) *pv = o.pv;
+    if (pi) *pi = o.pi;
+    return MPM_OK;
+}
+
+int mpm_affinity(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* ws,
+                 size_t ws_bytes, void* stream)
+{
+    int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off)) return MPM_ERR_INVALID_ARG;
+    Workspace w;
+    if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
+    return hip_status(mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, as_stream(stream)));
+}
+
+int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* nb,
+               float* best, void* ws, size_t ws_bytes, void* stream)
+{
+    int s = check_rows(B, N, D, dt);
     if (s != MPM_OK) return s;
     if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(nb) || !ok_opt_int_ptr(best))
         return MPM_ERR_INVALID_ARG;
-    return hip_status(mpm::launch_argmax(x, x_off, B, N, D, dt, nb, best, as_stream(stream)));
+    Workspace w;
+    if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
+    const hipStream_t st = as_stream(stream);
+    hipError_t e = mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, st);
+    if (e == hipSuccess) e = mpm::launch_reduce_partials(w.pv, w.pi, x, x_off, B, N, D, dt, nb, best, st);
+    return hip_status(e);
 }
 
 int mpm_pair_compact(const int32_t* nb, const int32_t* x_off, int32_t B, int32_t N, int32_t* map, int32_t* src,
@@ -106,6 +160,19 @@ int mpm_pair_compact(const int32_t* nb, const int32_t* x_off, int32_t B, int32_t
     if (!ok_int_ptr(nb) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(map) || !ok_int_ptr(src) || !ok_int_ptr(count))
         return MPM_ERR_INVALID_ARG;
     return hip_status(mpm::launch_pair_compact(nb, x_off, B, N, map, src, count, as_stream(stream)));
+}
+
+int mpm_pair_compact_ws(const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* map, void* ws,
+                        size_t ws_bytes, void* stream)
+{
+    int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!ok_opt_int_ptr(x_off) || !ok_int_ptr(map)) return MPM_ERR_INVALID_ARG;
+    Workspace w;
+    if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
+    return hip_status(mpm::launch_pair_compact_partials(w.pv, w.pi, mpm::partial_tiles(N),
+                                                        mpm::partial_tile_width(D, dt, N), w.nb, x_off, B, N, map,
+                                                        w.src, w.count, as_stream(stream)));
 }
 
 int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count, int32_t B,
@@ -119,25 +186,20 @@ int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, co
     return hip_status(mpm::launch_pair_average(x, x_off, src, count, B, N, D, dt, y, y_off, as_stream(stream)));
 }
 
-size_t mpm_merge_workspace_bytes(int32_t B, int32_t N)
-{
-    if (B < 1 || N < 1) return 0;
-    return workspace_bytes(B, N, nullptr, nullptr);
-}
-
 int mpm_merge(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* y,
               int32_t* y_off, int32_t* map, void* ws, size_t ws_bytes, void* stream)
 {
-    const int s = check_rows(B, N, D, dt);
+    int s = check_rows(B, N, D, dt);
     if (s != MPM_OK) return s;
-    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_rows_ptr(y) || !ok_int_ptr(y_off) || !ok_int_ptr(map) ||
-        ws == nullptr || !aligned(ws, kAlign))
+    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_rows_ptr(y) || !ok_int_ptr(y_off) || !ok_int_ptr(map))
         return MPM_ERR_INVALID_ARG;
-    MergeWorkspace w;
-    if (ws_bytes < workspace_bytes(B, N, &w, ws)) return MPM_ERR_WORKSPACE;
+    Workspace w;
+    if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     const hipStream_t st = as_stream(stream);
-    hipError_t e = mpm::launch_argmax(x, x_off, B, N, D, dt, w.nb, nullptr, st);
-    if (e == hipSuccess) e = mpm::launch_pair_compact(w.nb, x_off, B, N, map, w.src, w.count, st);
+    hipError_t e = mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, st);
+    if (e == hipSuccess)
+        e = mpm::launch_pair_compact_partials(w.pv, w.pi, mpm::partial_tiles(N), mpm::partial_tile_width(D, dt, N),
+                                              w.nb, x_off, B, N, map, w.src, w.count, st);
     if (e == hipSuccess) e = mpm::launch_pair_average(x, x_off, w.src, w.count, B, N, D, dt, y, y_off, st);
     return hip_status(e);
 }

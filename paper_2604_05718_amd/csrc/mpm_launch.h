@@ -9,8 +9,17 @@ namespace mpm {
 
 enum Dtype : int { kF32 = 0, kBf16 = 1 };
 
-hipError_t launch_argmax(const void* x, const int32_t* x_off, int B, int N, int D, int dt,
-                         int32_t* nb, float* best, hipStream_t stream);
+// Affinity + per-candidate-tile argmax partials: pv/pi are [B][partial_tiles(N)][N].
+hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, int D, int dt, float* pv,
+                           int32_t* pi, hipStream_t stream);
+int partial_tiles(int N);
+// Candidate rows covered by one partial of the kernel launch_affinity picks.
+int partial_tile_width(int D, int dt, int N);
+hipError_t launch_reduce_partials(const float* pv, const int32_t* pi, const void* x, const int32_t* x_off, int B,
+                                  int N, int D, int dt, int32_t* nb, float* best, hipStream_t stream);
+hipError_t launch_pair_compact_partials(const float* pv, const int32_t* pi, int T, int ct, int32_t* nb,
+                                        const int32_t* x_off, int B, int N, int32_t* map, int32_t* src,
+                                        int32_t* count, hipStream_t stream);
 
 hipError_t launch_pair_compact(const int32_t* nb, const int32_t* x_off, int B, int N,
                                int32_t* map, int32_t* src, int32_t* count, hipStream_t stream);

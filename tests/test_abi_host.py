@@ -32,11 +32,18 @@ def test_version_and_status_strings(lib):
     assert lib.mpm_last_hip_error() == 0
 
 
-def test_workspace_bytes(lib):
-    B, N = 64, 1024
+def test_workspace_bytes_and_offsets(lib):
     r = lambda v: (v + 255) // 256 * 256
-    assert lib.mpm_merge_workspace_bytes(B, N) == r(4 * B * N) + r(8 * B * N) + r(4 * B)
-    assert lib.mpm_merge_workspace_bytes(0, 5) == 0
+    for B, N in [(64, 1024), (16, 4096), (3, 5), (1, 257)]:
+        T = (N + 255) // 256
+        want = r(4 * B * N) + r(8 * B * N) + r(4 * B) + r(4 * B * T * N) + r(4 * B * T * N)
+        assert lib.mpm_workspace_bytes(B, N) == want
+        off = _lib.workspace_offsets(B, N)
+        assert off["nb"] == 0 and off["src"] == r(4 * B * N) and off["count"] == off["src"] + r(8 * B * N)
+        assert off["pv"] == off["count"] + r(4 * B) and off["pi"] == off["pv"] + r(4 * B * T * N)
+        assert all(v % 256 == 0 for v in off.values())
+    assert lib.mpm_workspace_bytes(0, 5) == 0
+    assert lib.mpm_workspace_offsets(0, 5, None, None, None, None, None) == 1
 
 
 @pytest.mark.parametrize("args,code", [
@@ -54,17 +61,24 @@ def test_workspace_bytes(lib):
     ((A, None, 2, 16, 16384 + 8, 1, A2, None), 2),  # D above MPM_MAX_D
 ])
 def test_argmax_rejects(lib, args, code):
-    assert lib.mpm_argmax(*args, None) == code
+    big = 1 << 40
+    assert lib.mpm_argmax(*args, A, big, None) == code
+    if args[6] is not None:  # the same rejection holds for the affinity step (which takes no nb)
+        assert lib.mpm_affinity(*args[:6], A, big, None) == code
 
 
-def test_merge_rejects(lib):
-    need = lib.mpm_merge_workspace_bytes(4, 64)
+def test_workspace_checks(lib):
+    need = lib.mpm_workspace_bytes(4, 64)
     ok = (A, None, 4, 64, 64, 1, A2, A2, A2, A, need)
     # Workspace one byte short.
     assert lib.mpm_merge(*ok[:10], need - 1, None) == 3
-    # Workspace not 256-byte aligned.
+    assert lib.mpm_affinity(A, None, 4, 64, 64, 1, A, need - 1, None) == 3
+    assert lib.mpm_argmax(A, None, 4, 64, 64, 1, A2, None, A, need - 1, None) == 3
+    assert lib.mpm_pair_compact_ws(None, 4, 64, 64, 1, A2, A, need - 1, None) == 3
+    # Workspace not 256-byte aligned, or missing.
     assert lib.mpm_merge(*ok[:9], ctypes.c_void_p(0x10010), need, None) == 1
     assert lib.mpm_merge(*ok[:9], None, need, None) == 1
+    assert lib.mpm_affinity(A, None, 4, 64, 64, 1, None, need, None) == 1
     # Null merged-token buffer.
     assert lib.mpm_merge(A, None, 4, 64, 64, 1, None, A2, A2, A, need, None) == 1
 

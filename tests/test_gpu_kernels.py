@@ -238,3 +238,31 @@ def test_deterministic_across_runs():
         assert torch.equal(sa.y[:n], sb.y[:n])
         n_in = torch.diff(sa.y_off.cpu())
     assert torch.equal(a.out, b.out)
+
+
+def test_step_entry_points_equal_merge_and_schedule():
+    """mpm_merge == mpm_affinity + mpm_pair_compact_ws + mpm_pair_average, and the
+    preallocated Schedule equals run_schedule, bit for bit (ragged stage 2)."""
+    from paper_2604_05718_amd import api
+
+    rng = np.random.default_rng(21)
+    B, N, D = 9, 600, 192
+    x = torch.stack([store(clustered(rng, N, D, k=15, sigma=0.3), "bf16") for _ in range(B)]).to(DEV)
+    ref = mpm.run_schedule(x, insertions=2)
+    sched = api.Schedule(B, N, D, torch.bfloat16, insertions=2)
+    for _ in range(2):  # the second run reuses the buffers
+        out = sched.run(x)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref.out) and torch.equal(sched.rstar, ref.rstar)
+    n_in = [N] * B
+    for s in range(2):
+        assert torch.equal(sched.map[s], ref.stages[s].map)
+        assert torch.equal(sched.y_off[s], ref.stages[s].y_off)
+        for b, n in enumerate(n_in):
+            assert torch.equal(sched.nb[s][b, :n], ref.stages[s].nb[b, :n])
+        rows = int(sched.y_off[s][-1])
+        assert torch.equal(sched.y[s][:rows], ref.stages[s].y[:rows])
+        n_in = torch.diff(sched.y_off[s].cpu()).tolist()
+    # The argmax step entry point agrees with the merge's neighbours.
+    nb = mpm.argmax(x)
+    assert torch.equal(nb, ref.stages[0].nb)
