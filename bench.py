@@ -31,7 +31,8 @@ METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak
 # HBM traffic of the affinity-argmax kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = None  # {"source_sha256": ..., "bytes_per_launch": ...}
+TRAFFIC = {"source_sha256": "c66db9892e878e80d4951d7fff1786aca0187977f51993206b520e49c4112307",
+           "bytes_per_launch": 95548325}
 
 
 def log(*a):
