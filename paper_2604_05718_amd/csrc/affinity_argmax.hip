@@ -129,7 +129,7 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
-    const int wave = tid / kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // wave-uniform: scalar registers and branches
     const int wc = wave % WC;
     const int wq = wave / WC;
     const int lrow = lane & 31;   // operand row inside a 32-row MFMA tile
@@ -356,7 +356,7 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
-    const int wave = tid / kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // wave-uniform: scalar registers and branches
     const int wc = wave % WC;
     const int wq = wave / WC;
     const int lrow = lane & 31;
@@ -410,10 +410,12 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
     // the issue cursor's item; they change per item, not per chunk.
     struct Offsets {
         uint32_t v[LOADS];
+        int group0;  // first row of this wave's load groups (uniform)
     };
     auto offsets_of = [&](const Item& it) {
         Offsets o;
-        const int first = (w_is_q ? it.qbase : it.cbase) + wr0 + lrow8;
+        o.group0 = (w_is_q ? it.qbase : it.cbase) + wr0;
+        const int first = o.group0 + lrow8;
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) {
             int row = first + i * 8;
@@ -427,6 +429,9 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
         const uint8_t* base = x + (long)it.row0 * rowbytes + (long)chunk * CB;   // uniform
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) {
+            // With a 2-stage ring every wait is vmcnt(0), so groups of 8 rows wholly past
+            // the image can be skipped (their LDS rows are never used unmasked).
+            if (STAGES == 2 && o.group0 + i * 8 >= it.n) continue;
             const uint32_t off = o.v[i];  // a non-dependent operand type keeps the host stub instantiable
             __builtin_amdgcn_global_load_lds(base + off, (__attribute__((address_space(3))) void*)(l0 + i * 8 * CB), 16,
                                              0, 0);
@@ -512,7 +517,14 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
         const float* iv = inv_c[par];
         const int n = ci.n;
         const int cb = ci.cbase;
-        const bool need_mask = (cb + CT > n) || (cb < ci.qbase + QT && ci.qbase < cb + CT);
+        // 32-row tiles of this wave that hold at least one token of the image (uniform);
+        // the others are computed on clamped rows and skipped here.
+        const int mt_lim = min(MT, max(0, (n - (cb + wc * MT * 32) + 31) / 32));
+        const int nt_lim = min(NT, max(0, (n - (ci.qbase + wq * NT * 32) + 31) / 32));
+        // With equal, aligned query and candidate tiles, a query's own index can only
+        // be a candidate when the two blocks coincide.
+        static_assert(CT == QT, "self exclusion assumes equal query and candidate tiles");
+        const bool diag = cb == ci.qbase;
         // Accumulator element r = 4g+e of this lane is candidate row 8g + 4*khalf + e of
         // its 32-row tile, so rows ascend with r. Each 16-value group is reduced by a
         // tournament in which the left (lower) entry wins ties, then merged into the
@@ -522,25 +534,36 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
         int32_t bi[NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-            const int qi = ci.qbase + wq * NT * 32 + nt * 32 + lrow;
-            float vb = -__builtin_inff();
-            int32_t jb = -1;
+            bv[nt] = -__builtin_inff();
+            bi[nt] = -1;
+        }
+        // This lane's own row inside a 32-row tile, as an accumulator element (if it holds it).
+        const int self_r = (((lrow >> 2) & 1) == khalf) ? 4 * (lrow >> 3) + (lrow & 3) : -1;
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                const int jt = cb + wc * MT * 32 + mt * 32 + 4 * khalf;  // candidate of r = 0
+        for (int mt = 0; mt < MT; ++mt) {
+            if (mt >= mt_lim) break;
+            const int jt = cb + wc * MT * 32 + mt * 32 + 4 * khalf;  // candidate of r = 0
+            f32x4 ivv[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                ivv[g] = *reinterpret_cast<const f32x4*>(&iv[wc * MT * 32 + mt * 32 + 8 * g + 4 * khalf]);
+            const bool partial = cb + wc * MT * 32 + mt * 32 + 32 > n;  // some rows of this tile are past the image
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                if (nt >= nt_lim) break;
                 float sc[16];
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const f32x4 ivv = *reinterpret_cast<const f32x4*>(&iv[wc * MT * 32 + mt * 32 + 8 * g + 4 * khalf]);
+                for (int g = 0; g < 4; ++g)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) sc[4 * g + e] = acc[mt][nt][4 * g + e] * ivv[e];
+                    for (int e = 0; e < 4; ++e) sc[4 * g + e] = acc[mt][nt][4 * g + e] * ivv[g][e];
+                if (partial) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        sc[r] = jt + 8 * (r >> 2) + (r & 3) < n ? sc[r] : -__builtin_inff();
                 }
-                if (need_mask) {
+                if (diag && wc * MT + mt == wq * NT + nt) {  // the tile holding each lane's own query
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int j = jt + 8 * (r >> 2) + (r & 3);
-                        sc[r] = (j < n && j != qi) ? sc[r] : -__builtin_inff();
-                    }
+                    for (int r = 0; r < 16; ++r) sc[r] = r == self_r ? -__builtin_inff() : sc[r];
                 }
                 float v8[8];
                 int r8[8];
@@ -567,17 +590,15 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
                 const bool cf = v21 > v20;
                 const float v1 = cf ? v21 : v20;
                 const int r1 = cf ? r21 : r20;
-                const bool up = v1 > vb;
-                vb = up ? v1 : vb;
-                jb = up ? jt + r1 + 4 * (r1 >> 2) : jb;  // row 8*(r/4) + r%4 of the tile
+                const bool up = v1 > bv[nt];
+                bv[nt] = up ? v1 : bv[nt];
+                bi[nt] = up ? jt + r1 + 4 * (r1 >> 2) : bi[nt];  // row 8*(r/4) + r%4 of the tile
             }
-            bv[nt] = vb;
-            bi[nt] = jb;
         }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x16{};
+            for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x16{};  // the next item starts from zero
         // Merge the two lane halves, then the WC candidate waves (larger score, then smaller index).
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {

@@ -266,3 +266,15 @@ def test_step_entry_points_equal_merge_and_schedule():
     # The argmax step entry point agrees with the merge's neighbours.
     nb = mpm.argmax(x)
     assert torch.equal(nb, ref.stages[0].nb)
+
+
+def test_many_items_per_workgroup():
+    """More images than workgroup slots (several work items per persistent
+    workgroup, full and ragged tiles), checked completely."""
+    rng = np.random.default_rng(33)
+    B, N, D = 40, 512, 128
+    x = torch.stack([store(clustered(rng, N, D, k=25, sigma=0.3), "bf16") for _ in range(B)])
+    res = mpm.run_schedule(x.to(DEV), insertions=2)
+    torch.cuda.synchronize()
+    for b in (0, 7, 8, 23, 39):
+        check_schedule_image(x[b], "bf16", res, b)
