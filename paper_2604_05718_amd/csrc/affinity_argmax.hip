@@ -323,18 +323,20 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
 // fetched from HBM once and re-read from that XCD's L2 by the other items that
 // use it, instead of being refetched once per candidate tile.
 //
-// LDS layout of one stage: CB = 128 bytes of K per row, rows of an operand
-// stored one after the other (128 B each), with the eight 16-byte columns of a
-// row permuted by an XOR swizzle: column c of row r sits in slot
-// c ^ swz(r), swz(r) = ((r % 8) / 2) | (((r / 8) % 2) << 2). One load instruction
-// fills 8 consecutive rows: lane l reads 16 bytes of row l/8 (8 lanes cover
-// one full 128-byte line of global memory) and lands at 16*l of a contiguous
-// 1 KB. An MFMA fragment read (rows r..r+31 of one 16-byte column per lane
-// half) then touches 16 distinct 16-byte bank groups in every 16-lane group,
-// so it is free of bank conflicts on the 64-bank LDS.
+// LDS layout of one stage: CB bytes of K per row (CB = 64 or 128), rows of an
+// operand stored one after the other, with the CB/16 16-byte columns of a row
+// permuted by an XOR swizzle: column c of row r sits in slot c ^ swz(r), with
+//   CB = 128: swz(r) = ((r % 8) / 2) | (((r / 8) % 2) << 2),
+//   CB =  64: swz(r) = (r / 4) % 4.
+// One load instruction fills 1 KB = 1024/CB consecutive rows: lane l reads 16
+// bytes of row l / (CB/16) (the lanes of a row cover its CB contiguous bytes of
+// global memory) and lands at 16*l. An MFMA fragment read (one 16-byte column
+// of 32 consecutive rows per lane half) then touches 16 distinct 16-byte bank
+// groups in every 16-lane group, so it is free of bank conflicts on the
+// 64-bank LDS. Load groups are dealt to the waves round-robin.
 // Rows past the image are clamped to its last row (their scores are masked).
-template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES>
-__global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
+template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES, bool DMA>
+__global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  // 2 waves per SIMD
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int T, int xcds,
     int slots, float* __restrict__ pv, int32_t* __restrict__ pi)
 {
@@ -342,10 +344,13 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
     constexpr int WAVES = WC * WQ;
     constexpr int CT = WC * MT * 32;
     constexpr int QT = WQ * NT * 32;
-    static_assert(CB == 128, "the swizzled layout assumes 128-byte row chunks");
-    constexpr int LOADS = (CT + QT) / 8 / WAVES;      // load instructions (8 rows each) per wave per stage
+    static_assert(CB == 64 || CB == 128, "swizzled layouts exist for 64- and 128-byte row chunks");
+    constexpr int NS = CB / 16;                       // 16-byte slots per row
+    constexpr int RPI = 64 / NS;                      // rows per load instruction (1 KB)
+    constexpr int GROUPS = (CT + QT) / RPI;           // load instructions per stage
+    constexpr int LOADS = GROUPS / WAVES;             // ... per wave
     constexpr int STAGE_BYTES = (CT + QT) * CB;
-    static_assert((CT + QT) / 8 % WAVES == 0, "stage/wave mismatch");
+    static_assert(GROUPS % WAVES == 0 && CT % RPI == 0 && CT % 32 == 0 && QT % 32 == 0, "stage/wave mismatch");
     static_assert((STAGES - 2) * LOADS < 64, "vmcnt range");
     static_assert(STAGES >= 2 && STAGES <= 5, "pipeline depth");
 
@@ -394,46 +399,55 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
     };
 
     // Swizzle of the 16-byte column slot for a row (see the layout note above).
-    auto swz = [](int r) { return ((r & 7) >> 1) | (((r >> 3) & 1) << 2); };
-    const int lrow8 = lane >> 3;                          // row inside an 8-row load group
-    const int lslot = lane & 7;                           // column slot this lane fills
-    // Each wave fills 8 * LOADS consecutive rows of one operand block; row r of
-    // a load group i has r % 8 == lrow8 and (r / 8) % 2 == i % 2, so its slot
-    // swizzle is one of two per-lane constants.
-    static_assert(CT % (8 * LOADS) == 0, "a wave's rows must not straddle the two operands");
-    const int wrow0 = wave * 8 * LOADS;                   // first row of this wave in [cand; query]
-    const bool w_is_q = wrow0 >= CT;
-    const int wr0 = w_is_q ? wrow0 - CT : wrow0;          // first row inside its operand block
-    const uint32_t col_even = (uint32_t)((lslot ^ (lrow8 >> 1)) << 4);
-    const uint32_t col_odd = (uint32_t)((lslot ^ (lrow8 >> 1) ^ 4) << 4);
+    auto swz = [](int r) {
+        return CB == 128 ? (((r & 7) >> 1) | (((r >> 3) & 1) << 2)) : ((r >> 2) & 3);
+    };
+    const int lrowi = lane / NS;                          // row inside a load group
+    const int lslot = lane % NS;                          // column slot this lane fills
+    // Load group u = wave + WAVES * i covers rows u*RPI .. u*RPI+RPI-1 of [cand; query].
     // Byte offsets (from the image's first row) of this lane's 16-byte pieces for
     // the issue cursor's item; they change per item, not per chunk.
     struct Offsets {
         uint32_t v[LOADS];
-        int group0;  // first row of this wave's load groups (uniform)
     };
     auto offsets_of = [&](const Item& it) {
         Offsets o;
-        o.group0 = (w_is_q ? it.qbase : it.cbase) + wr0;
-        const int first = o.group0 + lrow8;
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) {
-            int row = first + i * 8;
+            const int u = wave + WAVES * i;
+            const bool is_q = u * RPI >= CT;
+            const int r = u * RPI - (is_q ? CT : 0) + lrowi;   // row inside its operand block
+            int row = (is_q ? it.qbase : it.cbase) + r;
             row = row < it.n ? row : it.n - 1;
-            o.v[i] = (uint32_t)row * (uint32_t)rowbytes + ((i & 1) ? col_odd : col_even);
+            o.v[i] = (uint32_t)row * (uint32_t)rowbytes + (uint32_t)((lslot ^ swz(r & 15)) << 4);
         }
         return o;
     };
+    // Register staging (DMA == false): the next stage's 16-byte pieces wait in
+    // VGPRs while the current stage is consumed, and are written to LDS after it.
+    u32x4 stage_regs[DMA ? 1 : LOADS];
+    int stage_buf = 0;
     auto issue = [&](const Item& it, const Offsets& o, int chunk, int buf) {
-        uint8_t* l0 = lds + buf * STAGE_BYTES + wrow0 * CB;
+        uint8_t* sb = lds + buf * STAGE_BYTES;
         const uint8_t* base = x + (long)it.row0 * rowbytes + (long)chunk * CB;   // uniform
+        if (!DMA) {
+            stage_buf = buf;
+#pragma unroll
+            for (int i = 0; i < LOADS; ++i) {
+                const uint32_t off = o.v[i];
+                stage_regs[DMA ? 0 : i] = load16(base + off);
+            }
+            return;
+        }
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) {
-            // With a 2-stage ring every wait is vmcnt(0), so groups of 8 rows wholly past
-            // the image can be skipped (their LDS rows are never used unmasked).
-            if (STAGES == 2 && o.group0 + i * 8 >= it.n) continue;
+            const int u = wave + WAVES * i;
+            const bool is_q = u * RPI >= CT;
+            // With a 2-stage ring every wait is vmcnt(0), so groups wholly past the
+            // image can be skipped (their LDS rows are never used unmasked).
+            if (STAGES == 2 && (is_q ? it.qbase : it.cbase) + u * RPI - (is_q ? CT : 0) >= it.n) continue;
             const uint32_t off = o.v[i];  // a non-dependent operand type keeps the host stub instantiable
-            __builtin_amdgcn_global_load_lds(base + off, (__attribute__((address_space(3))) void*)(l0 + i * 8 * CB), 16,
+            __builtin_amdgcn_global_load_lds(base + off, (__attribute__((address_space(3))) void*)(sb + u * RPI * CB), 16,
                                              0, 0);
         }
     };
@@ -461,8 +475,15 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
             if (ii.k < nitems) ioff = offsets_of(ii);
         }
     };
+    auto commit = [&]() {
+        uint8_t* sb = lds + stage_buf * STAGE_BYTES;
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i)
+            *reinterpret_cast<u32x4*>(sb + (wave + WAVES * i) * RPI * CB + 16 * lane) = stage_regs[DMA ? 0 : i];
+    };
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s) issue_next();
+    if (!DMA && issued > 0) commit();
 
     Item ci = find(slot);  // compute cursor
     int cchunk = 0;
@@ -475,6 +496,7 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
         else if (STAGES > 3 && pending == 2) __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * LOADS) & 15) | (((2 * LOADS) >> 4) << 14));
         else if (STAGES > 2 && pending == 1) __builtin_amdgcn_s_waitcnt(0x0F70 | (LOADS & 15) | ((LOADS >> 4) << 14));
         else __builtin_amdgcn_s_waitcnt(0x0F70);
+        if (!DMA) __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0), lgkmcnt(0): this wave's LDS writes are done
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         issue_next();  // refills the buffer every wave finished reading last step
@@ -483,7 +505,7 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
         // Row lrow of every 32-row fragment has the same swizzle (32 is a multiple of 16).
         const uint8_t* lc = sbase + (wc * MT * 32 + lrow) * CB;
         const uint8_t* lq = sbase + (CT + wq * NT * 32 + lrow) * CB;
-        const int sw = swz(lrow);
+        const int sw = swz(lrow & 15);
 #pragma unroll
         for (int g = 0; g < CB / 32; ++g) {
             const int col = ((2 * g + khalf) ^ sw) << 4;
@@ -501,6 +523,7 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
             for (int mt = 0; mt < MT; ++mt)
                 if (mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(a[mt], ss[mt]);
         }
+        if (!DMA && issued > consumed + 1) commit();  // the next stage waits in registers: write it out
         ++consumed;
         if (++cchunk < nchunks) continue;
 
@@ -521,10 +544,12 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
         // the others are computed on clamped rows and skipped here.
         const int mt_lim = min(MT, max(0, (n - (cb + wc * MT * 32) + 31) / 32));
         const int nt_lim = min(NT, max(0, (n - (ci.qbase + wq * NT * 32) + 31) / 32));
-        // With equal, aligned query and candidate tiles, a query's own index can only
-        // be a candidate when the two blocks coincide.
-        static_assert(CT == QT, "self exclusion assumes equal query and candidate tiles");
-        const bool diag = cb == ci.qbase;
+        // Query blocks are aligned and no larger than candidate tiles, so a query's own
+        // index is a candidate of this item only when its block lies inside the tile;
+        // it then sits in candidate 32-row tile (qbase - cb)/32 + (query 32-row tile).
+        static_assert(CT % QT == 0, "query blocks must nest in candidate tiles");
+        const bool diag = ci.qbase >= cb && ci.qbase < cb + CT;
+        const int self_tile0 = (ci.qbase - cb) / 32;
         // Accumulator element r = 4g+e of this lane is candidate row 8g + 4*khalf + e of
         // its 32-row tile, so rows ascend with r. Each 16-value group is reduced by a
         // tournament in which the left (lower) entry wins ties, then merged into the
@@ -561,7 +586,7 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_partial_kernel(
                     for (int r = 0; r < 16; ++r)
                         sc[r] = jt + 8 * (r >> 2) + (r & 3) < n ? sc[r] : -__builtin_inff();
                 }
-                if (diag && wc * MT + mt == wq * NT + nt) {  // the tile holding each lane's own query
+                if (diag && wc * MT + mt == self_tile0 + wq * NT + nt) {  // the tile holding each lane's own query
 #pragma unroll
                     for (int r = 0; r < 16; ++r) sc[r] = r == self_r ? -__builtin_inff() : sc[r];
                 }
@@ -682,8 +707,10 @@ __global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __res
     }
 }
 
-// Persistent-kernel tile shape (bfloat16): 256 candidates x 256 queries on 8 waves.
-constexpr int kPWC = 2, kPWQ = 4, kPMT = 4, kPNT = 2, kPCB = 128, kPSTAGES = 2;
+// Persistent-kernel shape (bfloat16): 256 candidates x 256 queries on 8 waves,
+// 128-byte K chunks, double-buffered, one workgroup per CU.
+constexpr int kPWC = 2, kPWQ = 4, kPMT = 4, kPNT = 2, kPCB = 128, kPSTAGES = 2, kPWGS = 1;
+constexpr bool kPDMA = false;
 constexpr int kPCT = kPWC * kPMT * 32;
 
 bool use_persistent(int D, int dt) { return dt == kBf16 && (2L * D) % kPCB == 0; }
@@ -723,11 +750,12 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
     if (use_persistent(D, dt)) {
         const int cus = device_cus();
         if (cus <= 0) return hipErrorInvalidDevice;
-        // One workgroup per CU (the stage ring fills most of the LDS). With a
-        // batch of at least 8 images, group the workgroups by XCD.
+        // kPWGS workgroups per CU. With a batch of at least 8 images, group the
+        // workgroups by XCD.
         const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
-        const int slots = cus / xcds;
-        hipLaunchKernelGGL((affinity_partial_kernel<Bf16, kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES>), dim3(cus),
+        const int groups = cus * kPWGS;
+        const int slots = groups / xcds;
+        hipLaunchKernelGGL((affinity_partial_kernel<Bf16, kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES, kPDMA>), dim3(groups),
                            dim3(kPWC * kPWQ * kWave), 0, stream, static_cast<const uint8_t*>(x), x_off, B, N, D, T,
                            xcds, slots, pv, pi);
         return hipGetLastError();
