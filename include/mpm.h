@@ -116,6 +116,18 @@ int mpm_affinity(const void* x, const int32_t* x_off, int32_t B, int32_t N, int3
                  size_t ws_bytes, void* stream);
 
 /*
+ * mpm_affinity with its kernel's execution interval recorded into two events,
+ * for callers that time the dominant kernel of a step (telemetry, profiling)
+ * without adding stream commands between kernels. start_event / stop_event
+ * are hipEvent_t the caller created (timing enabled) and owns; either may be
+ * NULL. They are bound to the kernel's own dispatch (hipExtLaunchKernel), so
+ * hipEventElapsedTime(start, stop) is that kernel's duration. Same results,
+ * arguments and errors as mpm_affinity otherwise.
+ */
+int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* ws,
+                       size_t ws_bytes, void* start_event, void* stop_event, void* stream);
+
+/*
  * Nearest neighbours: mpm_affinity, then the reduction of the partials.
  *   nb[b*N + i] = argmax_{j != i, j < n_b} cos(x_i, x_j), lowest j on equal
  *                 scores; -1 when n_b == 1. Entries i >= n_b are not written.

@@ -187,10 +187,15 @@ class Schedule:
     insertion runs the three kernels of ``mpm_merge`` through its step entry
     points (affinity, compaction, average), so they can be timed one by one.
 
-    ``run(x, marks=None)``: when ``marks`` is a list of ``n_marks()``
-    torch.cuda.Event objects, event k is recorded on the current stream just
-    before kernel k (in ``kernel_names`` order) and the last one after the
-    gather, so consecutive events bracket single kernels."""
+    ``run(x, marks=None, affinity_events=None)``: when ``marks`` is a list of
+    ``n_marks()`` torch.cuda.Event objects, event k is recorded on the current
+    stream just before kernel k (in ``kernel_names`` order) and the last one
+    after the gather, so consecutive events bracket single kernels. When
+    ``affinity_events`` is a list of one (start, stop) pair of timing events
+    per insertion, each pair is bound to that insertion's affinity kernel
+    itself (``mpm_affinity_timed``): no stream command is added, and
+    ``start.elapsed_time(stop)`` is the kernel's duration. The events must have
+    been recorded once before (torch creates them lazily)."""
 
     def __init__(self, B: int, N: int, D: int, dtype: torch.dtype, insertions: int = 2, device="cuda"):
         if insertions < 1:
@@ -226,7 +231,7 @@ class Schedule:
     def n_marks(self) -> int:
         return len(self.kernel_names) + 1
 
-    def run(self, x: torch.Tensor, marks=None) -> torch.Tensor:
+    def run(self, x: torch.Tensor, marks=None, affinity_events=None) -> torch.Tensor:
         if x.shape != (self.B, self.N, self.D) or x.dtype != self.dtype or not x.is_contiguous():
             raise ValueError("input does not match the schedule's shape/dtype")
         lib, st, B, N, D, dt = self._lib, _stream(), self.B, self.N, self.D, self._dt
@@ -242,7 +247,13 @@ class Schedule:
         for s in range(self.insertions):
             ws = self.ws[s]
             mark()
-            _lib.check("mpm_affinity", lib.mpm_affinity(_p(cur), _p(cur_off), B, N, D, dt, _p(ws), ws.numel(), st))
+            if affinity_events is None:
+                _lib.check("mpm_affinity", lib.mpm_affinity(_p(cur), _p(cur_off), B, N, D, dt, _p(ws), ws.numel(), st))
+            else:
+                ev0, ev1 = affinity_events[s]
+                _lib.check("mpm_affinity_timed", lib.mpm_affinity_timed(_p(cur), _p(cur_off), B, N, D, dt, _p(ws),
+                                                                        ws.numel(), ev0.cuda_event, ev1.cuda_event,
+                                                                        st))
             mark()
             _lib.check("mpm_pair_compact_ws", lib.mpm_pair_compact_ws(_p(cur_off), B, N, D, dt, _p(self.map[s]),
                                                                       _p(ws), ws.numel(), st))

@@ -23,6 +23,8 @@
 // The candidate norms are accumulated from the same register fragments that
 // feed the MFMAs (one wave row per candidate slice), so X is read once per
 // tile and no separate normalisation pass exists.
+#include <hip/hip_ext.h>
+
 #include "mpm_device.h"
 #include "mpm_launch.h"
 
@@ -725,15 +727,15 @@ int device_cus()
 
 template <class S, int WC, int WQ, int MT, int NT, int CHUNK>
 hipError_t launch_staged(const void* x, const int32_t* x_off, int B, int N, int D, int T, float* pv, int32_t* pi,
-                         hipStream_t stream)
+                         hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
     constexpr int QT = WQ * NT * 32;
     const int qblocks = (N + QT - 1) / QT;
     const int xcd_major = B >= kXcds ? 1 : 0;
     const long groups = xcd_major ? (long)kXcds * ((B + kXcds - 1) / kXcds) * qblocks : (long)B * qblocks;
-    hipLaunchKernelGGL((affinity_argmax_kernel<S, WC, WQ, MT, NT, CHUNK>), dim3((unsigned)groups),
-                       dim3(WC * WQ * kWave), 0, stream, static_cast<const uint8_t*>(x), x_off, B, N, D, qblocks,
-                       xcd_major, T, pv, pi);
+    hipExtLaunchKernelGGL((affinity_argmax_kernel<S, WC, WQ, MT, NT, CHUNK>), dim3((unsigned)groups),
+                          dim3(WC * WQ * kWave), 0, stream, start, stop, 0, static_cast<const uint8_t*>(x), x_off, B, N,
+                          D, qblocks, xcd_major, T, pv, pi);
     return hipGetLastError();
 }
 
@@ -744,7 +746,7 @@ int partial_tiles(int N) { return (N + kPCT - 1) / kPCT; }
 int partial_tile_width(int D, int dt, int N) { return use_persistent(D, dt) ? kPCT : N; }
 
 hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, int D, int dt, float* pv, int32_t* pi,
-                           hipStream_t stream)
+                           hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
     const int T = partial_tiles(N);
     if (use_persistent(D, dt)) {
@@ -755,13 +757,13 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
         const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
         const int groups = cus * kPWGS;
         const int slots = groups / xcds;
-        hipLaunchKernelGGL((affinity_partial_kernel<Bf16, kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES, kPDMA>), dim3(groups),
-                           dim3(kPWC * kPWQ * kWave), 0, stream, static_cast<const uint8_t*>(x), x_off, B, N, D, T,
-                           xcds, slots, pv, pi);
+        hipExtLaunchKernelGGL((affinity_partial_kernel<Bf16, kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES, kPDMA>),
+                              dim3(groups), dim3(kPWC * kPWQ * kWave), 0, stream, start, stop, 0,
+                              static_cast<const uint8_t*>(x), x_off, B, N, D, T, xcds, slots, pv, pi);
         return hipGetLastError();
     }
-    if (dt == kBf16) return launch_staged<Bf16, 2, 4, 4, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream);
-    return launch_staged<F32, 2, 2, 2, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream);
+    if (dt == kBf16) return launch_staged<Bf16, 2, 4, 4, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream, start, stop);
+    return launch_staged<F32, 2, 2, 2, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream, start, stop);
 }
 
 hipError_t launch_reduce_partials(const float* pv, const int32_t* pi, const void* x, const int32_t* x_off, int B,

@@ -137,6 +137,18 @@ int mpm_affinity(const void* x, const int32_t* x_off, int32_t B, int32_t N, int3
     return hip_status(mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, as_stream(stream)));
 }
 
+int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* ws,
+                       size_t ws_bytes, void* start_event, void* stop_event, void* stream)
+{
+    int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off)) return MPM_ERR_INVALID_ARG;
+    Workspace w;
+    if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
+    return hip_status(mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, as_stream(stream),
+                                           static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event)));
+}
+
 int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* nb,
                float* best, void* ws, size_t ws_bytes, void* stream)
 {

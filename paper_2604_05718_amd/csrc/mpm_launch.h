@@ -10,8 +10,9 @@ namespace mpm {
 enum Dtype : int { kF32 = 0, kBf16 = 1 };
 
 // Affinity + per-candidate-tile argmax partials: pv/pi are [B][partial_tiles(N)][N].
+// start/stop (may be null) are bound to the kernel's own dispatch (hipExtLaunchKernel).
 hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, int D, int dt, float* pv,
-                           int32_t* pi, hipStream_t stream);
+                           int32_t* pi, hipStream_t stream, hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 int partial_tiles(int N);
 // Candidate rows covered by one partial of the kernel launch_affinity picks.
 int partial_tile_width(int D, int dt, int N);

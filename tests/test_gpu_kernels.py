@@ -268,6 +268,30 @@ def test_step_entry_points_equal_merge_and_schedule():
     assert torch.equal(nb, ref.stages[0].nb)
 
 
+def test_timed_schedule_equals_untimed():
+    """Binding timing events to the affinity dispatches (mpm_affinity_timed)
+    changes no result, and each pair measures a positive kernel duration."""
+    from paper_2604_05718_amd import api
+
+    rng = np.random.default_rng(22)
+    B, N, D = 9, 600, 192
+    x = torch.stack([store(clustered(rng, N, D, k=15, sigma=0.3), "bf16") for _ in range(B)]).to(DEV)
+    sched = api.Schedule(B, N, D, torch.bfloat16, insertions=2)
+    ref = sched.run(x).clone()
+    ref_map = [m.clone() for m in sched.map]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(2)]
+    for e0, e1 in ev:
+        e0.record()
+        e1.record()
+    out = sched.run(x, affinity_events=ev)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    for s in range(2):
+        assert torch.equal(sched.map[s], ref_map[s])
+        ms = ev[s][0].elapsed_time(ev[s][1])
+        assert 0.0 < ms < 1000.0
+
+
 def test_many_items_per_workgroup():
     """More images than workgroup slots (several work items per persistent
     workgroup, full and ragged tiles), checked completely."""
