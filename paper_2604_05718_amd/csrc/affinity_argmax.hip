@@ -325,6 +325,17 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
 // fetched from HBM once and re-read from that XCD's L2 by the other items that
 // use it, instead of being refetched once per candidate tile.
 //
+// Pipeline. The chunks of all the workgroup's items form one stream. Before
+// chunk c is consumed, this wave's loads of chunks up to c+1 have landed and a
+// barrier makes every wave's loads visible and retires the ring slot of chunk
+// c-1, which is then refilled with chunk c+STAGES-1. Within a chunk the MFMA
+// fragments are double-buffered: the fragments of the next k-group (for the
+// last k-group: of the next chunk, already visible) are requested before the
+// current k-group's MFMAs issue, so LDS latency hides behind the matrix cores.
+// The global->LDS loads are written as assembly: the compiler cannot tell which
+// ring slot they fill and would otherwise wait for all of them before every LDS
+// read; their completion is waited for explicitly (vmcnt) instead.
+//
 // LDS layout of one stage: CB bytes of K per row (CB = 64 or 128), rows of an
 // operand stored one after the other, with the CB/16 16-byte columns of a row
 // permuted by an XOR swizzle: column c of row r sits in slot c ^ swz(r), with
@@ -337,11 +348,12 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
 // groups in every 16-lane group, so it is free of bank conflicts on the
 // 64-bank LDS. Load groups are dealt to the waves round-robin.
 // Rows past the image are clamped to its last row (their scores are masked).
-template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES, bool DMA>
+template <int WC, int WQ, int MT, int NT, int CB, int STAGES>
 __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  // 2 waves per SIMD
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int T, int xcds,
     int slots, float* __restrict__ pv, int32_t* __restrict__ pi)
 {
+    using S = Bf16;
     constexpr int THREADS = WC * WQ * kWave;
     constexpr int WAVES = WC * WQ;
     constexpr int CT = WC * MT * 32;
@@ -352,12 +364,13 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     constexpr int GROUPS = (CT + QT) / RPI;           // load instructions per stage
     constexpr int LOADS = GROUPS / WAVES;             // ... per wave
     constexpr int STAGE_BYTES = (CT + QT) * CB;
+    constexpr int KG = CB / 32;                       // 32-byte k-groups (one MFMA k-step each) per chunk
     static_assert(GROUPS % WAVES == 0 && CT % RPI == 0 && CT % 32 == 0 && QT % 32 == 0, "stage/wave mismatch");
-    static_assert((STAGES - 2) * LOADS < 64, "vmcnt range");
-    static_assert(STAGES >= 2 && STAGES <= 5, "pipeline depth");
+    static_assert(STAGES >= 3 && (STAGES - 2) * LOADS < 64, "pipeline depth / vmcnt range");
+    static_assert(KG % 2 == 0, "the fragment double buffer alternates over an even number of k-groups");
 
     __shared__ __attribute__((aligned(1024))) uint8_t lds[STAGES * STAGE_BYTES];
-    __shared__ __attribute__((aligned(16))) float inv_c[2][CT];
+    __shared__ __attribute__((aligned(16))) float inv_c[CT];
     __shared__ float red_v[WC][QT];
     __shared__ int32_t red_i[WC][QT];
 
@@ -425,33 +438,43 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         }
         return o;
     };
-    // Register staging (DMA == false): the next stage's 16-byte pieces wait in
-    // VGPRs while the current stage is consumed, and are written to LDS after it.
-    u32x4 stage_regs[DMA ? 1 : LOADS];
-    int stage_buf = 0;
-    auto issue = [&](const Item& it, const Offsets& o, int chunk, int buf) {
-        uint8_t* sb = lds + buf * STAGE_BYTES;
-        const uint8_t* base = x + (long)it.row0 * rowbytes + (long)chunk * CB;   // uniform
-        if (!DMA) {
-            stage_buf = buf;
-#pragma unroll
-            for (int i = 0; i < LOADS; ++i) {
-                const uint32_t off = o.v[i];
-                stage_regs[DMA ? 0 : i] = load16(base + off);
-            }
-            return;
-        }
+
+    Item ii = find(slot);  // issue cursor
+    Offsets ioff = offsets_of(ii);
+    int ichunk = 0;
+    int issued = 0;
+    auto issue_next = [&]() {
+        if (ii.k >= nitems) return;
+        uint8_t* sb = lds + (issued % STAGES) * STAGE_BYTES;
+        const uint8_t* base = x + (long)ii.row0 * rowbytes + (long)ichunk * CB;   // uniform
 #pragma unroll
         for (int i = 0; i < LOADS; ++i) {
-            const int u = wave + WAVES * i;
-            const bool is_q = u * RPI >= CT;
-            // With a 2-stage ring every wait is vmcnt(0), so groups wholly past the
-            // image can be skipped (their LDS rows are never used unmasked).
-            if (STAGES == 2 && (is_q ? it.qbase : it.cbase) + u * RPI - (is_q ? CT : 0) >= it.n) continue;
-            const uint32_t off = o.v[i];  // a non-dependent operand type keeps the host stub instantiable
-            __builtin_amdgcn_global_load_lds(base + off, (__attribute__((address_space(3))) void*)(sb + u * RPI * CB), 16,
-                                             0, 0);
+            const uint32_t off = ioff.v[i];
+            const uint32_t m0 =
+                (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)(sb + (wave + WAVES * i) * RPI * CB);
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(off), "s"(base)
+                         : "memory", "m0");
         }
+        ++issued;
+        if (++ichunk == nchunks) {
+            ichunk = 0;
+            ii = find(ii.k + slots);
+            if (ii.k < nitems) ioff = offsets_of(ii);
+        }
+    };
+
+    // Row lrow of every 32-row fragment has the same swizzle (32 is a multiple of 16).
+    const int sw = swz(lrow & 15);
+    const int lc_off = (wc * MT * 32 + lrow) * CB;
+    const int lq_off = (CT + wq * NT * 32 + lrow) * CB;
+    u32x4 fa0[MT], fq0[NT], fa1[MT], fq1[NT];
+    auto read_frags = [&](u32x4 (&fa)[MT], u32x4 (&fq)[NT], int chunk, int g) {
+        const uint8_t* sb = lds + (chunk % STAGES) * STAGE_BYTES;
+        const int col = ((2 * g + khalf) ^ sw) << 4;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) fa[mt] = *reinterpret_cast<const u32x4*>(sb + lc_off + mt * 32 * CB + col);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) fq[nt] = *reinterpret_cast<const u32x4*>(sb + lq_off + nt * 32 * CB + col);
     };
 
     f32x16 acc[MT][NT];
@@ -462,84 +485,65 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     float ss[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) ss[mt] = 0.0f;
-
-    Item ii = find(slot);  // issue cursor
-    Offsets ioff = offsets_of(ii);
-    int ichunk = 0;
-    int issued = 0;
-    auto issue_next = [&]() {
-        if (ii.k >= nitems) return;
-        issue(ii, ioff, ichunk, issued % STAGES);
-        ++issued;
-        if (++ichunk == nchunks) {
-            ichunk = 0;
-            ii = find(ii.k + slots);
-            if (ii.k < nitems) ioff = offsets_of(ii);
-        }
-    };
-    auto commit = [&]() {
-        uint8_t* sb = lds + stage_buf * STAGE_BYTES;
+    auto mma = [&](const u32x4 (&fa)[MT], const u32x4 (&fq)[NT]) {
 #pragma unroll
-        for (int i = 0; i < LOADS; ++i)
-            *reinterpret_cast<u32x4*>(sb + (wave + WAVES * i) * RPI * CB + 16 * lane) = stage_regs[DMA ? 0 : i];
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) Mfma<S>::mma(acc[mt][nt], fa[mt], fq[nt]);
+        // Candidate norms: m-tile mt is summed by the wave with wq == mt % WQ only.
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            if (mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(fa[mt], ss[mt]);
     };
+    // vmcnt(n) with expcnt and lgkmcnt unconstrained.
+    constexpr int kWaitAhead = 0x0F70 | ((((STAGES - 2) * LOADS) & 15)) | ((((STAGES - 2) * LOADS) >> 4) << 14);
+
+    // Prologue: STAGES-1 chunks requested, chunk 0 landed and visible, its first fragments requested.
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s) issue_next();
-    if (!DMA && issued > 0) commit();
+    if (issued == STAGES - 1) __builtin_amdgcn_s_waitcnt(kWaitAhead);
+    else __builtin_amdgcn_s_waitcnt(0x0F70);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    read_frags(fa0, fq0, 0, 0);
 
     Item ci = find(slot);  // compute cursor
     int cchunk = 0;
     int consumed = 0;
-    int items_done = 0;
     while (ci.k < nitems) {
-        // Stages issued after the one consumed now may stay in flight.
-        const int pending = issued - consumed - 1;
-        if (pending >= STAGES - 2) __builtin_amdgcn_s_waitcnt(0x0F70 | (((STAGES - 2) * LOADS) & 15) | ((((STAGES - 2) * LOADS) >> 4) << 14));
-        else if (STAGES > 3 && pending == 2) __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * LOADS) & 15) | (((2 * LOADS) >> 4) << 14));
-        else if (STAGES > 2 && pending == 1) __builtin_amdgcn_s_waitcnt(0x0F70 | (LOADS & 15) | ((LOADS >> 4) << 14));
+        // This wave's loads of chunks up to c+1 have landed (later ones may stay in flight) ...
+        const int ahead = issued - consumed - 2;
+        if (ahead >= STAGES - 2) __builtin_amdgcn_s_waitcnt(kWaitAhead);
+        else if (STAGES > 3 && ahead == 1) __builtin_amdgcn_s_waitcnt(0x0F70 | (LOADS & 15) | ((LOADS >> 4) << 14));
         else __builtin_amdgcn_s_waitcnt(0x0F70);
-        if (!DMA) __builtin_amdgcn_s_waitcnt(0x0070);  // vmcnt(0), lgkmcnt(0): this wave's LDS writes are done
+        // ... every wave's are visible, and every wave is done with chunk c-1's slot.
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        issue_next();  // refills the buffer every wave finished reading last step
-
-        const uint8_t* sbase = lds + (consumed % STAGES) * STAGE_BYTES;
-        // Row lrow of every 32-row fragment has the same swizzle (32 is a multiple of 16).
-        const uint8_t* lc = sbase + (wc * MT * 32 + lrow) * CB;
-        const uint8_t* lq = sbase + (CT + wq * NT * 32 + lrow) * CB;
-        const int sw = swz(lrow & 15);
+        issue_next();
 #pragma unroll
-        for (int g = 0; g < CB / 32; ++g) {
-            const int col = ((2 * g + khalf) ^ sw) << 4;
-            u32x4 a[MT], q[NT];
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) a[mt] = *reinterpret_cast<const u32x4*>(lc + mt * 32 * CB + col);
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt) q[nt] = *reinterpret_cast<const u32x4*>(lq + nt * 32 * CB + col);
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) Mfma<S>::mma(acc[mt][nt], a[mt], q[nt]);
-            // Candidate norms: m-tile mt is summed by the wave with wq == mt % WQ only.
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                if (mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(a[mt], ss[mt]);
+        for (int g = 0; g < KG; ++g) {
+            if (g + 1 < KG) {
+                if ((g & 1) == 0) read_frags(fa1, fq1, consumed, g + 1);
+                else read_frags(fa0, fq0, consumed, g + 1);
+            } else if (issued > consumed + 1) {
+                read_frags(fa0, fq0, consumed + 1, 0);
+            }
+            if ((g & 1) == 0) mma(fa0, fq0);
+            else mma(fa1, fq1);
         }
-        if (!DMA && issued > consumed + 1) commit();  // the next stage waits in registers: write it out
         ++consumed;
         if (++cchunk < nchunks) continue;
 
         // ---- end of an item: norms, scores, per-query partial argmax ----
-        const int par = items_done & 1;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             if (mt % WQ != wq) continue;
             const float t = ss[mt] + __shfl_xor(ss[mt], 32);  // lanes l, l+32: the two k halves
             ss[mt] = 0.0f;
-            if (khalf == 0) inv_c[par][wc * MT * 32 + mt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+            if (khalf == 0) inv_c[wc * MT * 32 + mt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
         }
         lds_barrier();
-        const float* iv = inv_c[par];
+        const float* iv = inv_c;
         const int n = ci.n;
         const int cb = ci.cbase;
         // 32-row tiles of this wave that hold at least one token of the image (uniform);
@@ -663,7 +667,6 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
             pv[o] = v;
             pi[o] = i;
         }
-        ++items_done;
         cchunk = 0;
         ci = find(ci.k + slots);
     }
@@ -710,9 +713,8 @@ __global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __res
 }
 
 // Persistent-kernel shape (bfloat16): 256 candidates x 256 queries on 8 waves,
-// 128-byte K chunks, double-buffered, one workgroup per CU.
-constexpr int kPWC = 2, kPWQ = 4, kPMT = 4, kPNT = 2, kPCB = 128, kPSTAGES = 2, kPWGS = 1;
-constexpr bool kPDMA = false;
+// 64-byte K chunks in a 4-deep ring (128 KB of LDS), one workgroup per CU.
+constexpr int kPWC = 2, kPWQ = 4, kPMT = 4, kPNT = 2, kPCB = 64, kPSTAGES = 4, kPWGS = 1;
 constexpr int kPCT = kPWC * kPMT * 32;
 
 bool use_persistent(int D, int dt) { return dt == kBf16 && (2L * D) % kPCB == 0; }
@@ -757,7 +759,7 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
         const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
         const int groups = cus * kPWGS;
         const int slots = groups / xcds;
-        hipExtLaunchKernelGGL((affinity_partial_kernel<Bf16, kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES, kPDMA>),
+        hipExtLaunchKernelGGL((affinity_partial_kernel<kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES>),
                               dim3(groups), dim3(kPWC * kPWQ * kWave), 0, stream, start, stop, 0,
                               static_cast<const uint8_t*>(x), x_off, B, N, D, T, xcds, slots, pv, pi);
         return hipGetLastError();
