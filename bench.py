@@ -31,8 +31,8 @@ METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak
 # HBM traffic of the affinity-argmax kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "c66db9892e878e80d4951d7fff1786aca0187977f51993206b520e49c4112307",
-           "bytes_per_launch": 95548325}
+TRAFFIC = {"source_sha256": "7e251caee272a0a392f04c02bdd0a9f5ca0e1a849c6f96d7c3b63fb4483a0786",
+           "bytes_per_launch": 95595558}
 
 
 def log(*a):
