@@ -27,6 +27,7 @@ PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 matrix
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak"
+AFF_SAMPLE = 8   # every 8th timed step carries the affinity kernels' timing events
 
 # HBM traffic of the affinity-argmax kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
@@ -101,6 +102,8 @@ def main() -> int:
     ap.add_argument("--workload", default="vit_b_512")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the CPU oracle baseline (0 skips it)")
+    ap.add_argument("--cold-steps", type=int, default=10,
+                    help="steps timed after evicting the caches (0 skips them)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run 5 device-to-device copies of this many MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -141,11 +144,13 @@ def main() -> int:
     torch.cuda.synchronize()
     log(f"bench: warmup {args.warmup} done, timing {args.steps} steps")
 
-    # Timed region: K plain steps. The affinity kernels (the dominant kernel) are
-    # timed by events bound to their own dispatches, which adds no stream commands.
-    aff_ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(cfg.insertions)] for _ in range(args.steps)]
-    for pairs in aff_ev:
+    # Timed region: K steps. The affinity kernels (the dominant kernel) of every
+    # AFF_SAMPLE-th step are timed by events bound to their own dispatches; each such
+    # event costs a few microseconds of stream time, so only a sample carries them.
+    sampled = list(range(0, args.steps, AFF_SAMPLE))
+    aff_ev = {k: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(cfg.insertions)] for k in sampled}
+    for pairs in aff_ev.values():
         for e0, e1 in pairs:  # torch creates events lazily, at their first record
             e0.record()
             e1.record()
@@ -153,11 +158,11 @@ def main() -> int:
     torch.cuda.synchronize()
     start.record()
     for k in range(args.steps):
-        sched.run(x, affinity_events=aff_ev[k])
+        sched.run(x, affinity_events=aff_ev.get(k))
     end.record()
     torch.cuda.synchronize()
     ms_per_step = start.elapsed_time(end) / args.steps
-    aff_ms = [sum(pairs[s][0].elapsed_time(pairs[s][1]) for pairs in aff_ev) / args.steps
+    aff_ms = [sum(aff_ev[k][s][0].elapsed_time(aff_ev[k][s][1]) for k in sampled) / len(sampled)
               for s in range(cfg.insertions)]
     log(f"bench: {ms_per_step * 1e3:.1f} us/step, affinity kernels " + ", ".join(f"{m * 1e3:.1f}" for m in aff_ms) + " us")
 
@@ -177,6 +182,61 @@ def main() -> int:
     per_kernel_ms = [sum(m[i].elapsed_time(m[i + 1]) for m in marks) / args.steps for i in range(len(names))]
     counts = [torch.diff(sched.y_off[s].cpu()).tolist() for s in range(cfg.insertions)]
     work = algorithmic_work(cfg, counts)
+
+    # Step-time distribution: one event per step boundary (outside the timed region).
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    bounds[0].record()
+    for k in range(args.steps):
+        sched.run(x)
+        bounds[k + 1].record()
+    torch.cuda.synchronize()
+    step_ms = sorted(bounds[k].elapsed_time(bounds[k + 1]) for k in range(args.steps))
+    pct = lambda q: step_ms[min(len(step_ms) - 1, int(q * (len(step_ms) - 1) + 0.5))]
+    distribution = {"p10_ms": round(pct(0.1), 4), "median_ms": round(pct(0.5), 4), "p90_ms": round(pct(0.9), 4)}
+
+    # Cold caches: before each step a 1 GiB buffer is overwritten, which evicts the token
+    # matrix from the 256 MB MALL and the L2s; per-kernel events as in the breakdown loop.
+    cold = None
+    if args.cold_steps > 0:
+        scrub = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        cmarks = [[torch.cuda.Event(enable_timing=True) for _ in range(nm)] for _ in range(args.cold_steps)]
+        for k in range(args.cold_steps):
+            scrub.fill_(k & 0xFF)
+            sched.run(x, cmarks[k])
+        torch.cuda.synchronize()
+        del scrub
+        cold_kernel_ms = [sum(m[i].elapsed_time(m[i + 1]) for m in cmarks) / args.cold_steps
+                          for i in range(len(names))]
+        cold = {"steps": args.cold_steps,
+                "ms_per_step_with_per_kernel_events": round(sum(cold_kernel_ms), 4),
+                "kernels": []}
+        for name, ms, (kind, amount) in zip(names, cold_kernel_ms, work):
+            ent = {"name": name, "us": round(ms * 1e3, 2)}
+            if kind == "bytes":
+                gbs = amount / (ms * 1e-3) / 1e9
+                ent.update({"gbs": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
+            cold["kernels"].append(ent)
+
+    # The same step captured once in a HIP graph and replayed.
+    graph = None
+    try:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            sched.run(x)
+        for _ in range(3):
+            g.replay()
+        torch.cuda.synchronize()
+        gs, ge = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        gs.record()
+        for _ in range(args.steps):
+            g.replay()
+        ge.record()
+        torch.cuda.synchronize()
+        gms = gs.elapsed_time(ge) / args.steps
+        graph = {"ms_per_step": round(gms, 4), "images_per_s": round(cfg.B / (gms * 1e-3), 1)}
+        del g
+    except Exception as exc:  # reported, not fatal: the eager figures above stand on their own
+        graph = {"error": f"{type(exc).__name__}: {exc}"}
 
     kernels = []
     for name, ms, (kind, amount) in zip(names, per_kernel_ms, work):
@@ -220,10 +280,14 @@ def main() -> int:
                                 f"{cfg.insertions} MPM insertions + compose + gather"),
                    "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "none (1 GPU)"},
         "tokens_per_s": round(value * cfg.N, 0),
+        "affinity_timed_steps": len(sampled),
         "ms_per_step_with_per_kernel_events": round(ms_marked, 4),
         "survivors_mean": [round(sum(c) / len(c), 1) for c in counts],
         "roofline": roofline,
+        "step_time_distribution": distribution,
         "kernels": kernels,
+        "cold_cache": cold,
+        "hip_graph": graph,
     }
     if args.cpu_seconds > 0:
         log("bench: timing the CPU oracle baseline")
