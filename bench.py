@@ -61,14 +61,18 @@ def algorithmic_work(cfg, counts):
         # average: read every member row once, write every cluster row, read src
         work.append(("bytes", sum((n + m) * D * s + 8.0 * m for n, m in zip(n_in, n_out))))
         n_in = n_out
+    # gather: read the composed map, each final row once, write the full grid
+    gather = sum(4.0 * N + m * D * s + N * D * s for m in n_in)
     if cfg.insertions == 1:
         work.append(("bytes", 8.0 * N * B))
-    else:
-        # compose: read r* (4N), touch the stage map of the previous survivors (4 n), write r* (4N)
-        for st in range(1, cfg.insertions):
-            work.append(("bytes", sum(8.0 * N + 4.0 * m for m in counts[st - 1])))
-    # gather: read the composed map, each final row once, write the full grid
-    work.append(("bytes", sum(4.0 * N + m * D * s + N * D * s for m in n_in)))
+        work.append(("bytes", gather))
+        return work
+    # compose: read r* (4N), touch the stage map of the previous survivors (4 n), write r* (4N);
+    # the last composition runs inside the gather kernel
+    compose = [sum(8.0 * N + 4.0 * m for m in counts[st - 1]) for st in range(1, cfg.insertions)]
+    for c in compose[:-1]:
+        work.append(("bytes", c))
+    work.append(("bytes", compose[-1] + gather))
     return work
 
 

@@ -200,6 +200,18 @@ int mpm_compose(const int32_t* map_a, const int32_t* map_b, int32_t B, int32_t N
 int mpm_unmerge(const void* z, const int32_t* z_off, const int32_t* map, const void* z_spec, int32_t E,
                 int32_t B, int32_t N, int32_t D, int32_t dt, void* out, void* stream);
 
+/*
+ * Composition folded into the gather (Eq. 3 and Eq. 4 in one pass over the grid):
+ *   r*(i) = map_b[b*N + map_a[b*N + i]], or -1 where map_a[b*N + i] < 0;
+ *   out as mpm_unmerge with map = r*;
+ *   map_ab (optional, may be NULL) receives r* in slot layout.
+ * map_ab must not alias map_a or map_b (MPM_ERR_INVALID_ARG if it does). Other
+ * arguments and errors as mpm_unmerge and mpm_compose.
+ */
+int mpm_compose_unmerge(const void* z, const int32_t* z_off, const int32_t* map_a, const int32_t* map_b,
+                        int32_t* map_ab, const void* z_spec, int32_t E, int32_t B, int32_t N, int32_t D, int32_t dt,
+                        void* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -155,6 +155,25 @@ def unmerge(z, z_off, rmap, z_spec=None, out=None):
     return out
 
 
+def compose_unmerge(z, z_off, map_a, map_b, z_spec=None, out=None, map_ab=None):
+    """Eq. 3 folded into Eq. 4: gathers through r* = map_b[map_a] per image and
+    writes r* to ``map_ab`` (allocated if None). Returns (out, map_ab)."""
+    B, N = map_a.shape
+    if z.dim() == 3:
+        z = z.reshape(-1, z.shape[-1])
+    D = z.shape[1]
+    E = 0 if z_spec is None else z_spec.shape[1]
+    if out is None:
+        out = torch.empty((B, E + N, D), dtype=z.dtype, device=z.device)
+    if map_ab is None:
+        map_ab = torch.empty_like(map_a)
+    lib = _lib.load()
+    _lib.check("mpm_compose_unmerge", lib.mpm_compose_unmerge(_p(z), _p(z_off), _p(map_a), _p(map_b.contiguous()),
+                                                              _p(map_ab), _p(z_spec), E, B, N, D, _dt(z), _p(out),
+                                                              _stream()))
+    return out, map_ab
+
+
 @dataclass
 class ScheduleResult:
     stages: list          # Merged per insertion
@@ -213,6 +232,7 @@ class Schedule:
         self.y = [torch.empty((B * N, D), dtype=dtype, device=dev) for _ in range(insertions)]
         self.y_off = [torch.empty((B + 1,), **i32) for _ in range(insertions)]
         self.rstar = torch.empty((B, N), **i32)
+        self.rchain = torch.empty((B, N), **i32) if insertions > 2 else None  # maps composed before the last
         self.out = torch.empty((B, N, D), dtype=dtype, device=dev)
         self._lib = _lib.load()
         self._dt = _DTYPES[dtype]
@@ -223,10 +243,9 @@ class Schedule:
         for s in range(self.insertions):
             names += [f"affinity{s + 1}", f"compact{s + 1}", f"average{s + 1}"]
         if self.insertions == 1:
-            names += ["copy_map"]
-        else:
-            names += ["compose"] * (self.insertions - 1)
-        return names + ["unmerge"]
+            return names + ["copy_map", "unmerge"]
+        # the last composition runs inside the gather (mpm_compose_unmerge)
+        return names + ["compose"] * (self.insertions - 2) + ["compose+unmerge"]
 
     def n_marks(self) -> int:
         return len(self.kernel_names) + 1
@@ -265,15 +284,18 @@ class Schedule:
         if self.insertions == 1:
             mark()
             self.rstar.copy_(self.map[0])
-        else:
             mark()
-            _lib.check("mpm_compose", lib.mpm_compose(_p(self.map[0]), _p(self.map[1]), B, N, _p(self.rstar), st))
-            for s in range(2, self.insertions):
+            _lib.check("mpm_unmerge", lib.mpm_unmerge(_p(cur), _p(cur_off), _p(self.rstar), None, 0, B, N, D, dt,
+                                                      _p(self.out), st))
+        else:
+            first = self.map[0]
+            for s in range(1, self.insertions - 1):
                 mark()
-                _lib.check("mpm_compose", lib.mpm_compose(_p(self.rstar), _p(self.map[s]), B, N, _p(self.rstar),
-                                                          st))
-        mark()
-        _lib.check("mpm_unmerge", lib.mpm_unmerge(_p(cur), _p(cur_off), _p(self.rstar), None, 0, B, N, D, dt,
-                                                  _p(self.out), st))
+                _lib.check("mpm_compose", lib.mpm_compose(_p(first), _p(self.map[s]), B, N, _p(self.rchain), st))
+                first = self.rchain
+            mark()
+            _lib.check("mpm_compose_unmerge", lib.mpm_compose_unmerge(
+                _p(cur), _p(cur_off), _p(first), _p(self.map[-1]), _p(self.rstar), None, 0, B, N, D, dt,
+                _p(self.out), st))
         mark()
         return self.out

@@ -224,6 +224,23 @@ int mpm_compose(const int32_t* map_a, const int32_t* map_b, int32_t B, int32_t N
     return hip_status(mpm::launch_compose(map_a, map_b, B, N, map_ab, as_stream(stream)));
 }
 
+int mpm_compose_unmerge(const void* z, const int32_t* z_off, const int32_t* map_a, const int32_t* map_b,
+                        int32_t* map_ab, const void* z_spec, int32_t E, int32_t B, int32_t N, int32_t D, int32_t dt,
+                        void* out, void* stream)
+{
+    const int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (E < 0 || (E > 0 && !ok_rows_ptr(z_spec)) || (E == 0 && z_spec != nullptr && !aligned(z_spec, 16)))
+        return MPM_ERR_INVALID_ARG;
+    if ((long)E + N > MPM_MAX_N + (long)MPM_MAX_N) return MPM_ERR_UNSUPPORTED;
+    if (!ok_rows_ptr(z) || !ok_opt_int_ptr(z_off) || !ok_int_ptr(map_a) || !ok_int_ptr(map_b) ||
+        !ok_opt_int_ptr(map_ab) || !ok_rows_ptr(out))
+        return MPM_ERR_INVALID_ARG;
+    if (map_ab != nullptr && (map_ab == map_a || map_ab == map_b)) return MPM_ERR_INVALID_ARG;
+    return hip_status(mpm::launch_unmerge(z, z_off, map_a, z_spec, E, B, N, D, dt, out, as_stream(stream), map_b,
+                                          map_ab));
+}
+
 int mpm_unmerge(const void* z, const int32_t* z_off, const int32_t* map, const void* z_spec, int32_t E, int32_t B,
                 int32_t N, int32_t D, int32_t dt, void* out, void* stream)
 {

@@ -32,8 +32,10 @@ hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_
 hipError_t launch_compose(const int32_t* map_a, const int32_t* map_b, int B, int N,
                           int32_t* map_ab, hipStream_t stream);
 
+// map2 (may be null): gather through map2[map[i]] instead, writing that composed
+// entry to map_ab (may be null) once per token.
 hipError_t launch_unmerge(const void* z, const int32_t* z_off, const int32_t* map,
                           const void* z_spec, int E, int B, int N, int D, int dt, void* out,
-                          hipStream_t stream);
+                          hipStream_t stream, const int32_t* map2 = nullptr, int32_t* map_ab = nullptr);
 
 }  // namespace mpm

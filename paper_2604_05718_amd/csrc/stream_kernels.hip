@@ -95,10 +95,14 @@ __global__ __launch_bounds__(kRowThreads) void compose_kernel(const int32_t* map
     map_ab[t] = a < 0 ? -1 : map_b[b * N + a];
 }
 
+// Gather reconstruction. With map2 != nullptr the source of token i is the
+// composition map2[map[i]] (Eq. 3 folded into Eq. 4), and map_ab (if given)
+// receives that composed entry, written once per row.
 template <class S>
 __global__ __launch_bounds__(kRowThreads) void unmerge_kernel(
     const uint8_t* __restrict__ z, const int32_t* __restrict__ z_off, const int32_t* __restrict__ map,
-    const uint8_t* __restrict__ z_spec, int E, int N, int D, int rows_per_block, uint8_t* __restrict__ out)
+    const int32_t* __restrict__ map2, int32_t* __restrict__ map_ab, const uint8_t* __restrict__ z_spec, int E,
+    int N, int D, int rows_per_block, uint8_t* __restrict__ out)
 {
     const int b = blockIdx.y;
     const int rows = E + N;
@@ -109,13 +113,18 @@ __global__ __launch_bounds__(kRowThreads) void unmerge_kernel(
     const int vpr = (int)(rowbytes / 16);
     const uint8_t* zimg = z + (long)(z_off ? z_off[b] : b * N) * rowbytes;
     const int32_t* mapb = map + (long)b * N;
+    const int32_t* map2b = map2 ? map2 + (long)b * N : nullptr;
     uint8_t* oimg = out + (long)b * rows * rowbytes;
     for_each_vec((long)r0 * vpr, (long)r1 * vpr, vpr, [&](long r, int c) {
         u32x4 v = {0u, 0u, 0u, 0u};
         if (r < E) {
             v = load16(z_spec + ((long)b * E + r) * rowbytes + c * 16);
         } else {
-            const int m = mapb[r - E];
+            int m = mapb[r - E];
+            if (map2b) {
+                m = m < 0 ? -1 : map2b[m];
+                if (map_ab && c == 0) map_ab[(long)b * N + r - E] = m;
+            }
             if (m >= 0) v = load16(zimg + m * rowbytes + c * 16);
         }
         store16_stream(oimg + r * rowbytes + c * 16, v);
@@ -157,7 +166,7 @@ hipError_t launch_compose(const int32_t* map_a, const int32_t* map_b, int B, int
 }
 
 hipError_t launch_unmerge(const void* z, const int32_t* z_off, const int32_t* map, const void* z_spec, int E, int B,
-                          int N, int D, int dt, void* out, hipStream_t stream)
+                          int N, int D, int dt, void* out, hipStream_t stream, const int32_t* map2, int32_t* map_ab)
 {
     const long rowbytes = (long)D * (dt == kBf16 ? 2 : 4);
     const int rpb = rows_per_block_for(rowbytes);
@@ -166,11 +175,11 @@ hipError_t launch_unmerge(const void* z, const int32_t* z_off, const int32_t* ma
     const uint8_t* sp = static_cast<const uint8_t*>(z_spec);
     uint8_t* op = static_cast<uint8_t*>(out);
     if (dt == kBf16)
-        hipLaunchKernelGGL(unmerge_kernel<Bf16>, grid, dim3(kRowThreads), 0, stream, zp, z_off, map, sp, E, N, D, rpb,
-                           op);
+        hipLaunchKernelGGL(unmerge_kernel<Bf16>, grid, dim3(kRowThreads), 0, stream, zp, z_off, map, map2, map_ab, sp, E,
+                           N, D, rpb, op);
     else
-        hipLaunchKernelGGL(unmerge_kernel<F32>, grid, dim3(kRowThreads), 0, stream, zp, z_off, map, sp, E, N, D, rpb,
-                           op);
+        hipLaunchKernelGGL(unmerge_kernel<F32>, grid, dim3(kRowThreads), 0, stream, zp, z_off, map, map2, map_ab, sp, E,
+                           N, D, rpb, op);
     return hipGetLastError();
 }
 

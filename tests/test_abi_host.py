@@ -92,4 +92,12 @@ def test_other_entry_points_reject(lib):
     assert lib.mpm_unmerge(A, None, A, None, -1, 2, 8, 64, 1, A, None) == 1   # E < 0
     assert lib.mpm_unmerge(A, None, A, None, 2, 2, 8, 64, 1, A, None) == 1    # E > 0 needs z_spec
     assert lib.mpm_unmerge(A, None, A, None, 0, 2, 8, 64, 1, None, None) == 1
+    # compose + gather: the same checks, plus the composed map must not alias an input map
+    A3 = ctypes.c_void_p(0x30000)
+    assert lib.mpm_compose_unmerge(A, None, A, A2, A3, None, -1, 2, 8, 64, 1, A, None) == 1   # E < 0
+    assert lib.mpm_compose_unmerge(A, None, A, None, A3, None, 0, 2, 8, 64, 1, A, None) == 1  # map_b NULL
+    assert lib.mpm_compose_unmerge(A, None, A, A2, A, None, 0, 2, 8, 64, 1, A, None) == 1     # map_ab == map_a
+    assert lib.mpm_compose_unmerge(A, None, A, A2, A2, None, 0, 2, 8, 64, 1, A, None) == 1    # map_ab == map_b
+    assert lib.mpm_compose_unmerge(A, None, A, A2, A3, None, 0, 2, 8, 63, 1, A, None) == 1    # D % 8 (bf16)
+    assert lib.mpm_compose_unmerge(A, None, A, A2, A3, None, 0, 2, 16385, 64, 1, A, None) == 2
     assert lib.mpm_last_hip_error() == 0

@@ -199,6 +199,51 @@ def test_compose_and_unmerge_with_special_rows():
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("packed,E", [(True, 2), (False, 0), (True, 0)])
+def test_compose_unmerge_matches_compose_then_unmerge(dtype, packed, E):
+    """mpm_compose_unmerge (Eq. 3 folded into Eq. 4) equals mpm_compose followed by
+    mpm_unmerge bit for bit, against the oracle's composition, and works with the
+    composed-map output omitted (NULL)."""
+    from paper_2604_05718_amd import _lib, api
+
+    rng = np.random.default_rng(11)
+    B, N, D = 4, 200, 40
+    n1s = [150, 200, 1, 97]
+    n2s = [110, 133, 1, 60]
+    r1 = np.full((B, N), -1, np.int32)
+    r2 = np.full((B, N), -1, np.int32)
+    for b in range(B):
+        r1[b] = np.concatenate([np.arange(n1s[b]), rng.integers(0, n1s[b], N - n1s[b])])
+        r2[b, : n1s[b]] = np.concatenate([np.arange(n2s[b]), rng.integers(0, n2s[b], n1s[b] - n2s[b])])
+    r1[3, 11] = -1  # a slot outside the image
+    tdt = TORCH_DT[dtype]
+    if packed:
+        z = torch.randn(sum(n2s), D).to(tdt).to(DEV)
+        z_off = torch.from_numpy(np.concatenate([[0], np.cumsum(n2s)]).astype(np.int32)).to(DEV)
+    else:
+        z = torch.randn(B * N, D).to(tdt).to(DEV)
+        z_off = None
+    spec = torch.randn(B, E, D).to(tdt).to(DEV) if E else None
+    m1 = torch.from_numpy(r1).to(DEV)
+    m2 = torch.from_numpy(r2).to(DEV)
+    ref_r = mpm.compose(m1, m2)
+    ref = mpm.unmerge(z, z_off, ref_r, z_spec=spec)
+    out, rstar = api.compose_unmerge(z, z_off, m1, m2, z_spec=spec)
+    out2 = torch.full_like(out, 7)
+    lib = _lib.load()
+    _lib.check("mpm_compose_unmerge", lib.mpm_compose_unmerge(
+        api._p(z), api._p(z_off), api._p(m1), api._p(m2), None, api._p(spec), E, B, N, D,
+        _lib.MPM_BF16 if dtype == "bf16" else _lib.MPM_F32, api._p(out2), api._stream()))
+    torch.cuda.synchronize()
+    assert torch.equal(rstar, ref_r)
+    assert torch.equal(out, ref)
+    assert torch.equal(out2, ref)
+    rs = rstar.cpu().numpy()
+    for b in range(B):
+        assert np.array_equal(rs[b], oracle.compose(r1[b], r2[b]))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_duplicated_patches_closed_form(dtype):
     """Exact 2x2 duplicates: N1 = 3N/4, N2 = N/2, exact reconstruction."""
     G, D = 16, 64
