@@ -311,8 +311,9 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
     }
 }
 
-// Persistent variant for bfloat16 rows that are a whole number of CB-byte
-// chunks. Work item = (image, query block of QT, candidate tile of CT); an item
+// Persistent variant for rows (bfloat16 or float32) that are a whole number of
+// CB-byte chunks; everything below is laid out in bytes, and Mfma<S> consumes
+// the same 16-byte fragments for either type. Work item = (image, query block of QT, candidate tile of CT); an item
 // streams its two operand blocks through a STAGES-deep ring of LDS buffers
 // filled by direct global->LDS loads (global_load_lds_dwordx4), runs the K loop
 // on MFMA, then reduces its tile to one (score, index) partial per query.
@@ -348,12 +349,11 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
 // groups in every 16-lane group, so it is free of bank conflicts on the
 // 64-bank LDS. Load groups are dealt to the waves round-robin.
 // Rows past the image are clamped to its last row (their scores are masked).
-template <int WC, int WQ, int MT, int NT, int CB, int STAGES>
+template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES>
 __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  // 2 waves per SIMD
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int T, int xcds,
     int slots, float* __restrict__ pv, int32_t* __restrict__ pi)
 {
-    using S = Bf16;
     constexpr int THREADS = WC * WQ * kWave;
     constexpr int WAVES = WC * WQ;
     constexpr int CT = WC * MT * 32;
@@ -712,12 +712,12 @@ __global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __res
     }
 }
 
-// Persistent-kernel shape (bfloat16): 256 candidates x 256 queries on 8 waves,
-// 64-byte K chunks in a 4-deep ring (128 KB of LDS), one workgroup per CU.
+// Persistent-kernel shape: 256 candidates x 256 queries on 8 waves, 64-byte K
+// chunks in a 4-deep ring (128 KB of LDS), one workgroup per CU.
 constexpr int kPWC = 2, kPWQ = 4, kPMT = 4, kPNT = 2, kPCB = 64, kPSTAGES = 4, kPWGS = 1;
 constexpr int kPCT = kPWC * kPMT * 32;
 
-bool use_persistent(int D, int dt) { return dt == kBf16 && (2L * D) % kPCB == 0; }
+bool use_persistent(int D, int dt) { return ((long)D * (dt == kBf16 ? 2 : 4)) % kPCB == 0; }
 
 int device_cus()
 {
@@ -759,9 +759,14 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
         const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
         const int groups = cus * kPWGS;
         const int slots = groups / xcds;
-        hipExtLaunchKernelGGL((affinity_partial_kernel<kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES>),
-                              dim3(groups), dim3(kPWC * kPWQ * kWave), 0, stream, start, stop, 0,
-                              static_cast<const uint8_t*>(x), x_off, B, N, D, T, xcds, slots, pv, pi);
+        if (dt == kBf16)
+            hipExtLaunchKernelGGL((affinity_partial_kernel<Bf16, kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES>),
+                                  dim3(groups), dim3(kPWC * kPWQ * kWave), 0, stream, start, stop, 0,
+                                  static_cast<const uint8_t*>(x), x_off, B, N, D, T, xcds, slots, pv, pi);
+        else
+            hipExtLaunchKernelGGL((affinity_partial_kernel<F32, kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES>),
+                                  dim3(groups), dim3(kPWC * kPWQ * kWave), 0, stream, start, stop, 0,
+                                  static_cast<const uint8_t*>(x), x_off, B, N, D, T, xcds, slots, pv, pi);
         return hipGetLastError();
     }
     if (dt == kBf16) return launch_staged<Bf16, 2, 4, 4, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream, start, stop);
