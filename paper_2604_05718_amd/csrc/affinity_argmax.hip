@@ -620,7 +620,11 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                 const int r21 = c1 ? r4[3] : r4[2];
                 const bool cf = v21 > v20;
                 const float v1 = cf ? v21 : v20;
-                const int r1 = cf ? r21 : r20;
+                int r1 = cf ? r21 : r20;
+                // Materialise the winning index before the merge: otherwise the compiler moves
+                // the index selection into a divergent branch per tile, which serialises the
+                // tiles' tournaments (measured slower).
+                asm volatile("" : "+v"(r1));
                 const bool up = v1 > bv[nt];
                 bv[nt] = up ? v1 : bv[nt];
                 bi[nt] = up ? jt + r1 + 4 * (r1 >> 2) : bi[nt];  // row 8*(r/4) + r%4 of the tile

@@ -13,7 +13,9 @@ namespace mpm {
 namespace {
 
 constexpr int kRowThreads = 256;
-constexpr int kRowBytesPerBlock = 32768;  // output bytes one workgroup handles
+constexpr int kRowBytesPerBlock = 32768;     // output bytes one workgroup handles
+constexpr int kGatherBytesPerBlock = 16384;  // ... in the gather, which first resolves its rows' sources
+constexpr int kMaxRowsPerBlock = 4096;       // rows one gather workgroup resolves into LDS (16 KB)
 
 // Walks the flat range [f0, f1) of 16-byte vectors of a row-major block whose
 // rows hold `vpr` vectors, calling body(row, vec) with a stride of the
@@ -97,13 +99,16 @@ __global__ __launch_bounds__(kRowThreads) void compose_kernel(const int32_t* map
 
 // Gather reconstruction. With map2 != nullptr the source of token i is the
 // composition map2[map[i]] (Eq. 3 folded into Eq. 4), and map_ab (if given)
-// receives that composed entry, written once per row.
+// receives that composed entry. The workgroup first resolves the source row of
+// each of its output rows into LDS (one map lookup per row, not per vector),
+// then streams the rows' 16-byte vectors.
 template <class S>
 __global__ __launch_bounds__(kRowThreads) void unmerge_kernel(
     const uint8_t* __restrict__ z, const int32_t* __restrict__ z_off, const int32_t* __restrict__ map,
     const int32_t* __restrict__ map2, int32_t* __restrict__ map_ab, const uint8_t* __restrict__ z_spec, int E,
     int N, int D, int rows_per_block, uint8_t* __restrict__ out)
 {
+    __shared__ int32_t src_row[kMaxRowsPerBlock];
     const int b = blockIdx.y;
     const int rows = E + N;
     const int r0 = blockIdx.x * rows_per_block;
@@ -115,26 +120,34 @@ __global__ __launch_bounds__(kRowThreads) void unmerge_kernel(
     const int32_t* mapb = map + (long)b * N;
     const int32_t* map2b = map2 ? map2 + (long)b * N : nullptr;
     uint8_t* oimg = out + (long)b * rows * rowbytes;
+    for (int r = r0 + (int)threadIdx.x; r < r1; r += kRowThreads) {
+        int m = -1;  // special rows are not looked up
+        if (r >= E) {
+            m = mapb[r - E];
+            if (map2b) {
+                m = m < 0 ? -1 : map2b[m];
+                if (map_ab) map_ab[(long)b * N + r - E] = m;
+            }
+        }
+        src_row[r - r0] = m;
+    }
+    __syncthreads();
     for_each_vec((long)r0 * vpr, (long)r1 * vpr, vpr, [&](long r, int c) {
         u32x4 v = {0u, 0u, 0u, 0u};
         if (r < E) {
             v = load16(z_spec + ((long)b * E + r) * rowbytes + c * 16);
         } else {
-            int m = mapb[r - E];
-            if (map2b) {
-                m = m < 0 ? -1 : map2b[m];
-                if (map_ab && c == 0) map_ab[(long)b * N + r - E] = m;
-            }
+            const int m = src_row[r - r0];
             if (m >= 0) v = load16(zimg + m * rowbytes + c * 16);
         }
         store16_stream(oimg + r * rowbytes + c * 16, v);
     });
 }
 
-int rows_per_block_for(long rowbytes)
+int rows_per_block_for(long rowbytes, long block_bytes = kRowBytesPerBlock)
 {
-    const long r = kRowBytesPerBlock / rowbytes;
-    return r < 1 ? 1 : (int)r;
+    const long r = block_bytes / rowbytes;
+    return r < 1 ? 1 : (r > kMaxRowsPerBlock ? kMaxRowsPerBlock : (int)r);
 }
 
 }  // namespace
@@ -169,7 +182,7 @@ hipError_t launch_unmerge(const void* z, const int32_t* z_off, const int32_t* ma
                           int N, int D, int dt, void* out, hipStream_t stream, const int32_t* map2, int32_t* map_ab)
 {
     const long rowbytes = (long)D * (dt == kBf16 ? 2 : 4);
-    const int rpb = rows_per_block_for(rowbytes);
+    const int rpb = rows_per_block_for(rowbytes, kGatherBytesPerBlock);
     dim3 grid((E + N + rpb - 1) / rpb, B);
     const uint8_t* zp = static_cast<const uint8_t*>(z);
     const uint8_t* sp = static_cast<const uint8_t*>(z_spec);
