@@ -88,6 +88,24 @@ int carve(void* ws, size_t ws_bytes, int32_t B, int32_t N, Workspace* w)
 
 hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
+// nb from the affinity partials, then mutual pairs and compact ids. With few
+// candidate tiles the compaction kernel (one workgroup per image) reduces the
+// partials itself; with more, that serial reduction dominates, so a fully
+// parallel reduction writes nb first and the compaction reads it.
+constexpr int kFusedReduceMaxTiles = 4;
+
+hipError_t compact_from_partials(const Workspace& w, const int32_t* x_off, int32_t B, int32_t N, int32_t D,
+                                 int32_t dt, int32_t* map, hipStream_t st)
+{
+    const int T = mpm::partial_tiles(N);
+    const int ct = mpm::partial_tile_width(D, dt, N);
+    if ((N + ct - 1) / ct <= kFusedReduceMaxTiles)
+        return mpm::launch_pair_compact_partials(w.pv, w.pi, T, ct, w.nb, x_off, B, N, map, w.src, w.count, st);
+    hipError_t e = mpm::launch_reduce_partials(w.pv, w.pi, nullptr, x_off, B, N, D, dt, w.nb, nullptr, st);
+    if (e == hipSuccess) e = mpm::launch_pair_compact(w.nb, x_off, B, N, map, w.src, w.count, st);
+    return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -182,9 +200,7 @@ int mpm_pair_compact_ws(const int32_t* x_off, int32_t B, int32_t N, int32_t D, i
     if (!ok_opt_int_ptr(x_off) || !ok_int_ptr(map)) return MPM_ERR_INVALID_ARG;
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
-    return hip_status(mpm::launch_pair_compact_partials(w.pv, w.pi, mpm::partial_tiles(N),
-                                                        mpm::partial_tile_width(D, dt, N), w.nb, x_off, B, N, map,
-                                                        w.src, w.count, as_stream(stream)));
+    return hip_status(compact_from_partials(w, x_off, B, N, D, dt, map, as_stream(stream)));
 }
 
 int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count, int32_t B,
@@ -210,8 +226,7 @@ int mpm_merge(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t
     const hipStream_t st = as_stream(stream);
     hipError_t e = mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, st);
     if (e == hipSuccess)
-        e = mpm::launch_pair_compact_partials(w.pv, w.pi, mpm::partial_tiles(N), mpm::partial_tile_width(D, dt, N),
-                                              w.nb, x_off, B, N, map, w.src, w.count, st);
+        e = compact_from_partials(w, x_off, B, N, D, dt, map, st);
     if (e == hipSuccess) e = mpm::launch_pair_average(x, x_off, w.src, w.count, B, N, D, dt, y, y_off, st);
     return hip_status(e);
 }
