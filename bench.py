@@ -32,8 +32,8 @@ AFF_SAMPLE = 8   # every 8th timed step carries the affinity kernels' timing eve
 # HBM traffic of the affinity-argmax kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "7e251caee272a0a392f04c02bdd0a9f5ca0e1a849c6f96d7c3b63fb4483a0786",
-           "bytes_per_launch": 95595558}
+TRAFFIC = {"source_sha256": "6281c45da57df6ee5cebdb21b503dd1d0f777fa6d30d76250ed9ba48d1e2e211",
+           "bytes_per_launch": 95575299}
 
 
 def log(*a):
