@@ -93,9 +93,20 @@ def cpu_baseline(cfg, x_cpu, budget_s: float):
         "unit": "images/s",
         "cores": threads,
         "kind": "oracle",
+        "cpu": cpu_model(),
         "sample": (f"first {done} of {cfg.B} images of {cfg.name}, full schedule ({cfg.insertions} insertions, "
                    f"compose, gather), float64 brute force, {el:.1f} s"),
     }
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main() -> int:

@@ -368,6 +368,28 @@ def test_graph_replay_matches_eager():
             assert torch.equal(sched.map[s], ref_maps[s]), f"replay {rep} stage {s}"
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_merge_with_many_candidate_tiles(dtype):
+    """N above 1024 gives more than four candidate-tile partials per token, which
+    takes the parallel partial reduction before the compaction scan; a packed
+    ragged batch (every image a different length) through mpm_merge, checked
+    against the oracle stage by stage."""
+    rng = np.random.default_rng(41)
+    N, D = 1400, 64
+    ns = [1400, 1311, 1025, 7]
+    rows = [store(clustered(rng, n, D, k=40, sigma=0.3), dtype) for n in ns]
+    off = np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)
+    x = torch.cat(rows).to(DEV)
+    res = mpm.merge(x, torch.from_numpy(off).to(DEV), N=N)
+    torch.cuda.synchronize()
+    m = res.map.cpu().numpy()
+    nb = res.nb.cpu().numpy()
+    y = res.y.cpu()
+    y_off = res.y_off.cpu().numpy()
+    for b, n in enumerate(ns):
+        check_stage(to64(rows[b]), dtype, nb[b, :n], m[b], to64(y[y_off[b]:y_off[b + 1]]))
+
+
 def test_many_items_per_workgroup():
     """More images than workgroup slots (several work items per persistent
     workgroup, full and ragged tiles), checked completely."""
