@@ -32,8 +32,8 @@ AFF_SAMPLE = 8   # every 8th timed step carries the affinity kernels' timing eve
 # HBM traffic of the affinity-argmax kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "6281c45da57df6ee5cebdb21b503dd1d0f777fa6d30d76250ed9ba48d1e2e211",
-           "bytes_per_launch": 95575299}
+TRAFFIC = {"source_sha256": "2b4e2dfffee0079b76fea8ed3e13d53a5fbce9aa1558e6eab96b06fe50a5f0ca",
+           "bytes_per_launch": 106196464}
 
 
 def log(*a):
@@ -44,6 +44,22 @@ def kernel_source_hash() -> str:
     """Hash of the affinity kernel's source, to tell whether stored counters still apply."""
     p = os.path.join(ROOT, "paper_2604_05718_amd", "csrc", "affinity_argmax.hip")
     return hashlib.sha256(open(p, "rb").read()).hexdigest()
+
+
+def executed_affinity_flops(cfg, counts, schedule):
+    """Matrix-core flops each affinity launch issues: 2 * 256^2 * D per 256 x 256
+    block, nb^2 blocks per image of nb = ceil(n / 256) blocks under the full
+    schedule, nb (nb + 1) / 2 under the symmetric one (padding rows included)."""
+    out = []
+    n_in = [cfg.N] * cfg.B
+    for st in range(cfg.insertions):
+        blocks = 0
+        for n in n_in:
+            nb = (n + 255) // 256
+            blocks += nb * (nb + 1) // 2 if schedule == "symmetric" else nb * nb
+        out.append(blocks * 2.0 * 256 * 256 * cfg.D)
+        n_in = counts[st]
+    return out
 
 
 def algorithmic_work(cfg, counts):
@@ -253,13 +269,16 @@ def main() -> int:
     except Exception as exc:  # reported, not fatal: the eager figures above stand on their own
         graph = {"error": f"{type(exc).__name__}: {exc}"}
 
+    schedule = mpm.affinity_schedule_used(cfg.B, cfg.N, cfg.D, dtype)
+    executed = executed_affinity_flops(cfg, counts, schedule)
     kernels = []
     for name, ms, (kind, amount) in zip(names, per_kernel_ms, work):
         ent = {"name": name, "us": round(ms * 1e3, 2)}
         if kind == "flops":
             tf = amount / (ms * 1e-3) / 1e12
             peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
-            ent.update({"gflop": round(amount / 1e9, 3), "tflops": round(tf, 1), "frac_mfma": round(tf / peak, 4)})
+            ent.update({"gflop": round(amount / 1e9, 3), "tflops": round(tf, 1), "frac_mfma": round(tf / peak, 4),
+                        "executed_gflop": round(executed[int(name[len("affinity"):]) - 1] / 1e9, 3)})
         else:
             gbs = amount / (ms * 1e-3) / 1e9
             ent.update({"mbytes": round(amount / 1e6, 3), "gbs": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
@@ -274,8 +293,13 @@ def main() -> int:
     traffic = None
     if TRAFFIC and TRAFFIC.get("source_sha256") == kernel_source_hash():
         traffic = TRAFFIC["bytes_per_launch"]
+    # The same launches counted by the matrix-core work they issue: below the
+    # algorithmic figure under the symmetric schedule, which skips the blocks
+    # below the diagonal.
+    issued = sum(executed) / len(a_idx) / (a_ms / len(a_idx) * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": traffic}
+                "frac": round(achieved / peak, 4), "traffic": traffic, "schedule": schedule,
+                "issued": round(issued, 1), "frac_issued": round(issued / peak, 4)}
 
     value = cfg.B / (ms_per_step * 1e-3)
     result = {

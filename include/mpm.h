@@ -68,6 +68,12 @@ typedef enum {
     MPM_BF16 = 1   /* bfloat16 storage, float32 accumulation */
 } mpm_dtype;
 
+typedef enum {
+    MPM_SCHEDULE_AUTO = 0,      /* symmetric when it needs fewer work rounds (default) */
+    MPM_SCHEDULE_FULL = 1,      /* every (query block, candidate tile) pair */
+    MPM_SCHEDULE_SYMMETRIC = 2  /* pairs on and above the block diagonal only */
+} mpm_schedule;
+
 #define MPM_MAX_N 16384   /* tokens per image */
 #define MPM_MAX_B 65535   /* images per call */
 #define MPM_MAX_D 16384   /* channels per token */
@@ -126,6 +132,36 @@ int mpm_affinity(const void* x, const int32_t* x_off, int32_t B, int32_t N, int3
  */
 int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* ws,
                        size_t ws_bytes, void* start_event, void* stop_event, void* stream);
+
+/*
+ * Work schedule of the affinity kernel, for tuning and testing; results do not
+ * depend on it (the partials are bit-identical). The affinity of an image is
+ * symmetric (Eq. 1), so the symmetric schedule computes only the 256 x 256
+ * blocks on and above the block diagonal and takes each off-diagonal block's
+ * argmax in both directions, about half the matrix-core work for large images
+ * at the price of a cross-lane reduction per block. MPM_SCHEDULE_AUTO (the
+ * default) picks it when it needs fewer work rounds on the device's compute
+ * units. Applies to bfloat16 and float32 rows whose byte length is a multiple
+ * of 64 (other rows use a kernel without a schedule choice). Process-wide: it
+ * affects every later call on any thread; calls already enqueued are not
+ * changed. Returns the previous mode, or -1 (changing nothing) when `mode` is
+ * not an mpm_schedule value.
+ */
+int mpm_set_affinity_schedule(int32_t mode);
+
+/*
+ * The schedule (MPM_SCHEDULE_FULL or MPM_SCHEDULE_SYMMETRIC, never AUTO) that
+ * mpm_affinity would run for B images of at most N tokens of D channels of
+ * dtype dt on the current device under the current mode, written to
+ * *schedule (a host pointer). For reporting the matrix-core work a call
+ * issues: about 2 * 256^2 * D flops per 256 x 256 block, nb^2 blocks per
+ * image of nb = ceil(n_b / 256) blocks under the full schedule and
+ * nb (nb + 1) / 2 under the symmetric one. Rows whose byte length is not a
+ * multiple of 64 always report MPM_SCHEDULE_FULL. Returns MPM_OK,
+ * MPM_ERR_INVALID_ARG for bad sizes or a NULL pointer, or MPM_ERR_HIP when
+ * the device cannot be queried.
+ */
+int mpm_affinity_schedule_used(int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* schedule);
 
 /*
  * Nearest neighbours: mpm_affinity, then the reduction of the partials.

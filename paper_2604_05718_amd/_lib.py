@@ -20,6 +20,9 @@ MPM_ERR_WORKSPACE = 3
 MPM_ERR_HIP = 4
 MPM_F32 = 0
 MPM_BF16 = 1
+MPM_SCHEDULE_AUTO = 0
+MPM_SCHEDULE_FULL = 1
+MPM_SCHEDULE_SYMMETRIC = 2
 
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32
@@ -36,6 +39,8 @@ SIGNATURES = {
     "mpm_workspace_offsets": (ctypes.c_int, [_i32, _i32, _szp, _szp, _szp, _szp, _szp]),
     "mpm_affinity": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp]),
     "mpm_affinity_timed": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp, _vp, _vp]),
+    "mpm_set_affinity_schedule": (ctypes.c_int, [_i32]),
+    "mpm_affinity_schedule_used": (ctypes.c_int, [_i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_int32)]),
     "mpm_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "mpm_pair_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
     "mpm_pair_compact_ws": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),

@@ -103,6 +103,29 @@ def workspace_bytes(B: int, N: int) -> int:
     return int(_lib.load().mpm_workspace_bytes(B, N))
 
 
+SCHEDULES = {"auto": _lib.MPM_SCHEDULE_AUTO, "full": _lib.MPM_SCHEDULE_FULL, "symmetric": _lib.MPM_SCHEDULE_SYMMETRIC}
+
+
+def set_affinity_schedule(mode: str) -> str:
+    """Select the affinity kernel's work schedule ("auto", "full" or "symmetric",
+    process-wide); returns the previous one. Results do not depend on it."""
+    if mode not in SCHEDULES:
+        raise ValueError(f"unknown schedule {mode!r}; expected one of {sorted(SCHEDULES)}")
+    prev = _lib.load().mpm_set_affinity_schedule(SCHEDULES[mode])
+    if prev < 0:
+        raise _lib.MPMError("mpm_set_affinity_schedule", _lib.MPM_ERR_INVALID_ARG)
+    return {v: k for k, v in SCHEDULES.items()}[prev]
+
+
+def affinity_schedule_used(B: int, N: int, D: int, dtype: torch.dtype) -> str:
+    """The schedule ("full" or "symmetric") the affinity kernel runs for this shape
+    on the current device under the current mode."""
+    out = ctypes.c_int32()
+    _lib.check("mpm_affinity_schedule_used",
+               _lib.load().mpm_affinity_schedule_used(B, N, D, _DTYPES[dtype], ctypes.byref(out)))
+    return {v: k for k, v in SCHEDULES.items()}[out.value]
+
+
 @dataclass
 class Merged:
     y: torch.Tensor       # [B*N, D] packed merged tokens (rows beyond y_off[B] unused)

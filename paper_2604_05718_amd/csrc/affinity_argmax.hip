@@ -25,6 +25,8 @@
 // tile and no separate normalisation pass exists.
 #include <hip/hip_ext.h>
 
+#include <atomic>
+
 #include "mpm_device.h"
 #include "mpm_launch.h"
 
@@ -311,6 +313,42 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
     }
 }
 
+// Lane exchanges for the reverse-direction argmax of the symmetric schedule.
+// Each DPP pattern used is an involution on the lanes of a 16-lane row.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ int32_t dpp_i(int32_t x)
+{
+    return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
+}
+// (v, i) = the lexicographic maximum of (av, ai) and (bv, bi): larger score, then
+// smaller index (as unsigned, so -1 loses every tie). Branch-free.
+__device__ __forceinline__ void merge_pair(float& v, int32_t& i, float av, int32_t ai, float bv, int32_t bi)
+{
+    const bool c = (bv > av) | ((bv == av) & ((uint32_t)bi < (uint32_t)ai));
+    v = c ? bv : av;
+    i = c ? bi : ai;
+}
+// One reduce-scatter step over the H slot pairs (k, k+H): the partner lane (DPP
+// pattern CTRL) keeps the other half. Lanes with `upper` keep slots k+H, the others
+// slots k; each kept slot is merged with the partner's copy of it into slot k.
+template <int CTRL, int H>
+__device__ __forceinline__ void exchange_half(float* v, int32_t* ix, int upper)
+{
+#pragma unroll
+    for (int k = 0; k < H; ++k) {
+        const float kv = upper ? v[k + H] : v[k];
+        const int32_t ki = upper ? ix[k + H] : ix[k];
+        const float sv = upper ? v[k] : v[k + H];
+        const int32_t si = upper ? ix[k] : ix[k + H];
+        merge_pair(v[k], ix[k], kv, ki, dpp_f<CTRL>(sv), dpp_i<CTRL>(si));
+    }
+}
+
 // Persistent variant for rows (bfloat16 or float32) that are a whole number of
 // CB-byte chunks; everything below is laid out in bytes, and Mfma<S> consumes
 // the same 16-byte fragments for either type. Work item = (image, query block of QT, candidate tile of CT); an item
@@ -349,7 +387,19 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
 // groups in every 16-lane group, so it is free of bank conflicts on the
 // 64-bank LDS. Load groups are dealt to the waves round-robin.
 // Rows past the image are clamped to its last row (their scores are masked).
-template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES>
+//
+// Symmetric schedule (SYM). S = X X^T of an image is symmetric (Eq. 1), so only
+// the blocks with query block <= candidate tile are computed: nb(nb+1)/2 items
+// per image instead of nb^2. An off-diagonal item also yields the reverse
+// direction: each candidate row j of the tile gets its best query q of the block,
+// scored (x_j . x_q) * inv_q from the same accumulators, and writes the partial of
+// row j for tile slot "query block". Every (row, slot) partial is still written
+// exactly once, so the reduction over slots is unchanged. The products and sums
+// are the same as in the item that would compute block (j's tile, q's block)
+// directly, so the partials are bit-identical to the full schedule's. Items are
+// taken image by image, the blocks of an image row by row, so all the items of
+// an image still run together on one XCD and share its L2.
+template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES, bool SYM>
 __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  // 2 waves per SIMD
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int T, int xcds,
     int slots, float* __restrict__ pv, int32_t* __restrict__ pi)
@@ -373,6 +423,10 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     __shared__ __attribute__((aligned(16))) float inv_c[CT];
     __shared__ float red_v[WC][QT];
     __shared__ int32_t red_i[WC][QT];
+    __shared__ __attribute__((aligned(16))) float inv_q[SYM ? QT : 1];
+    __shared__ float red_cv[SYM ? WQ : 1][SYM ? CT : 1];
+    __shared__ int32_t red_ci[SYM ? WQ : 1][SYM ? CT : 1];
+    static_assert(!SYM || QT == CT, "the symmetric schedule pairs equal blocks");
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
@@ -384,7 +438,8 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
 
     const int group = blockIdx.x % xcds;
     const int slot = blockIdx.x / xcds;
-    const int per_img = ((N + QT - 1) / QT) * T;
+    const int nqb = (N + QT - 1) / QT;
+    const int per_img = SYM ? nqb * (nqb + 1) / 2 : nqb * T;
     const int nimg = (B - group + xcds - 1) / xcds;
     const int nitems = nimg * per_img;
     const long rowbytes = (long)D * S::kBytes;
@@ -398,10 +453,20 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         Item it;
         for (; k < nitems; k += slots) {
             const int ib = k / per_img;
-            const int w = k - ib * per_img;
+            int w = k - ib * per_img;
+            int qb, t;
+            if (SYM) {  // blocks qb <= t of the upper triangle, row by row
+                qb = 0;
+                while (w >= nqb - qb) {
+                    w -= nqb - qb;
+                    ++qb;
+                }
+                t = qb + w;
+            } else {
+                qb = w / T;
+                t = w - qb * T;
+            }
             const int b = group + xcds * ib;
-            const int qb = w / T;
-            const int t = w - qb * T;
             const int row0 = x_off ? x_off[b] : b * N;
             const int n = x_off ? x_off[b + 1] - row0 : N;
             if (qb * QT < n && t * CT < n) {
@@ -485,6 +550,9 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     float ss[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) ss[mt] = 0.0f;
+    float sq[NT];  // query norms (symmetric schedule only)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) sq[nt] = 0.0f;
     auto mma = [&](const u32x4 (&fa)[MT], const u32x4 (&fq)[NT]) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
@@ -494,6 +562,12 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
             if (mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(fa[mt], ss[mt]);
+        if constexpr (SYM) {
+            // Query norms, for the reverse direction: n-tile nt is summed by the wave with wc == nt % WC.
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                if (nt % WC == wc) sq[nt] = Mfma<S>::sumsq(fq[nt], sq[nt]);
+        }
     };
     // vmcnt(n) with expcnt and lgkmcnt unconstrained.
     constexpr int kWaitAhead = 0x0F70 | ((((STAGES - 2) * LOADS) & 15)) | ((((STAGES - 2) * LOADS) >> 4) << 14);
@@ -541,6 +615,15 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
             const float t = ss[mt] + __shfl_xor(ss[mt], 32);  // lanes l, l+32: the two k halves
             ss[mt] = 0.0f;
             if (khalf == 0) inv_c[wc * MT * 32 + mt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+        }
+        if constexpr (SYM) {
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                if (nt % WC != wc) continue;
+                const float t = sq[nt] + __shfl_xor(sq[nt], 32);
+                sq[nt] = 0.0f;
+                if (khalf == 0) inv_q[wq * NT * 32 + nt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+            }
         }
         lds_barrier();
         const float* iv = inv_c;
@@ -630,6 +713,84 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                 bi[nt] = up ? jt + r1 + 4 * (r1 >> 2) : bi[nt];  // row 8*(r/4) + r%4 of the tile
             }
         }
+        // Reverse direction of an off-diagonal item (query block before the candidate
+        // tile). A candidate row's queries of one n-tile sit in the 32 lanes of one lane
+        // half (one per lane), so after an in-lane merge over the NT n-tiles the best of
+        // each row is found by a reduce-scatter across the half: exchanges with lane
+        // l^16, l^15, l^7, l^2 and l^1 (XOR masks spanning all five lane bits) each
+        // halve the rows a lane carries, until lanes 2r and 2r+1 hold row r's best.
+        // Merges are lexicographic (larger score, then smaller query), so the lowest
+        // query wins ties, as in the forward direction.
+        const bool rev = SYM && !diag;
+        if (rev) {
+            float ivq[NT];
+            bool qok[NT];
+            int32_t qidx[NT];
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                const int ql = wq * NT * 32 + nt * 32 + lrow;
+                ivq[nt] = inv_q[ql];
+                qidx[nt] = ci.qbase + ql;
+                qok[nt] = qidx[nt] < n;
+            }
+            const bool all_q = ci.qbase + (wq + 1) * NT * 32 <= n;  // every query of this wave is a token (uniform)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                if (mt >= mt_lim) break;
+                // This lane's best query for each of its 16 accumulator rows (a strict >
+                // keeps the lower n-tile, i.e. the lower query, on ties).
+                float v[16];
+                int32_t ix[16];
+                if (all_q) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        v[r] = acc[mt][0][r] * ivq[0];
+                        ix[r] = qidx[0];
+#pragma unroll
+                        for (int nt = 1; nt < NT; ++nt) {
+                            const float s2 = acc[mt][nt][r] * ivq[nt];
+                            const bool c = s2 > v[r];
+                            v[r] = c ? s2 : v[r];
+                            ix[r] = c ? qidx[nt] : ix[r];
+                        }
+                    }
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        v[r] = qok[0] ? acc[mt][0][r] * ivq[0] : -__builtin_inff();
+                        ix[r] = qidx[0];
+#pragma unroll
+                        for (int nt = 1; nt < NT; ++nt) {
+                            const float s2 = qok[nt] ? acc[mt][nt][r] * ivq[nt] : -__builtin_inff();
+                            const bool c = s2 > v[r];
+                            v[r] = c ? s2 : v[r];
+                            ix[r] = c ? qidx[nt] : ix[r];
+                        }
+                    }
+                }
+                // l^16 with v_permlane16_swap: slots k and k+8 of the two 16-lane rows of a
+                // half trade places, and the lower row keeps rows k, the upper rows k+8.
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const auto sv = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[k]), __float_as_uint(v[k + 8]),
+                                                                     false, false);
+                    const auto si = __builtin_amdgcn_permlane16_swap((uint32_t)ix[k], (uint32_t)ix[k + 8], false, false);
+                    merge_pair(v[k], ix[k], __uint_as_float(sv[0]), (int32_t)si[0], __uint_as_float(sv[1]),
+                               (int32_t)si[1]);
+                }
+                exchange_half<0x140, 4>(v, ix, (lane >> 3) & 1);  // l^15 (row mirror), split on lane bit 3
+                exchange_half<0x141, 2>(v, ix, (lane >> 2) & 1);  // l^7 (half-row mirror), bit 2
+                exchange_half<0x4E, 1>(v, ix, (lane >> 1) & 1);   // l^2 (quad permutation 2,3,0,1), bit 1
+                merge_pair(v[0], ix[0], v[0], ix[0], dpp_f<0xB1>(v[0]), dpp_i<0xB1>(ix[0]));  // l^1 (1,0,3,2)
+                // Lanes 2r, 2r+1 of half h: accumulator row r = candidate row 8(r/4) + 4h + r%4.
+                if ((lane & 1) == 0) {
+                    const int r = (lrow >> 1) & 15;
+                    const int jl = wc * MT * 32 + mt * 32 + 8 * (r >> 2) + 4 * khalf + (r & 3);
+                    red_cv[wq][jl] = v[0];
+                    red_ci[wq][jl] = ix[0];
+                }
+            }
+        }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -670,6 +831,21 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
             const long o = ((long)ci.b * T + t) * N + qi;
             pv[o] = v;
             pi[o] = i;
+        }
+        if (rev) {
+            // Candidate rows of the tile over the query block: tile slot qbase / QT of their partials.
+            const int tq = ci.qbase / QT;
+            for (int jl = tid; jl < CT; jl += THREADS) {
+                const int j = cb + jl;
+                if (j >= n) continue;
+                float v = red_cv[0][jl];
+                int32_t i = red_ci[0][jl];
+#pragma unroll
+                for (int w = 1; w < WQ; ++w) merge_pair(v, i, v, i, red_cv[w][jl], red_ci[w][jl]);
+                const long o = ((long)ci.b * T + tq) * N + j;
+                pv[o] = v;
+                pi[o] = i;
+            }
         }
         cchunk = 0;
         ci = find(ci.k + slots);
@@ -717,9 +893,18 @@ __global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __res
 }
 
 // Persistent-kernel shape: 256 candidates x 256 queries on 8 waves, 64-byte K
-// chunks in a 4-deep ring (128 KB of LDS), one workgroup per CU.
+// chunks in a 4-deep ring (128 KB of LDS), one workgroup per CU. The full
+// schedule splits the tile over 2 candidate x 4 query waves (128 x 64 each); the
+// symmetric one over 4 x 2 (64 x 128 each), so that its reverse direction merges 4
+// queries inside each lane before the cross-lane steps and carries half as many
+// rows through them.
 constexpr int kPWC = 2, kPWQ = 4, kPMT = 4, kPNT = 2, kPCB = 64, kPSTAGES = 4, kPWGS = 1;
+constexpr int kSWC = 4, kSWQ = 2, kSMT = 2, kSNT = 4;
 constexpr int kPCT = kPWC * kPMT * 32;
+static_assert(kSWC * kSMT * 32 == kPCT && kSWQ * kSNT * 32 == kPCT && kPWQ * kPNT * 32 == kPCT,
+              "both schedules use 256 x 256 tiles, so their partials share one layout");
+
+std::atomic<int> g_schedule{kScheduleAuto};
 
 bool use_persistent(int D, int dt) { return ((long)D * (dt == kBf16 ? 2 : 4)) % kPCB == 0; }
 
@@ -729,6 +914,15 @@ int device_cus()
     if (hipGetDevice(&dev) != hipSuccess) return 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
     return cus;
+}
+
+template <class S, int WC, int WQ, int MT, int NT, bool SYM>
+void launch_persistent(const void* x, const int32_t* x_off, int B, int N, int D, int T, int xcds, int groups,
+                       float* pv, int32_t* pi, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
+{
+    hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB, kPSTAGES, SYM>), dim3(groups),
+                          dim3(WC * WQ * kWave), 0, stream, start, stop, 0, static_cast<const uint8_t*>(x), x_off, B,
+                          N, D, T, xcds, groups / xcds, pv, pi);
 }
 
 template <class S, int WC, int WQ, int MT, int NT, int CHUNK>
@@ -751,6 +945,37 @@ int partial_tiles(int N) { return (N + kPCT - 1) / kPCT; }
 
 int partial_tile_width(int D, int dt, int N) { return use_persistent(D, dt) ? kPCT : N; }
 
+int set_affinity_schedule(int mode)
+{
+    if (mode != kScheduleAuto && mode != kScheduleFull && mode != kScheduleSymmetric) return -1;
+    return g_schedule.exchange(mode);
+}
+
+bool symmetric_schedule(int B, int N, int xcds, int slots)
+{
+    const int mode = g_schedule.load();
+    if (mode != kScheduleAuto) return mode == kScheduleSymmetric;
+    // Rounds of work items per workgroup slot under either schedule. An off-diagonal
+    // item of the symmetric one costs about a fifth more (its reverse direction), so
+    // it pays only when it saves more than that in rounds.
+    const long nqb = (N + kPCT - 1) / kPCT;
+    const long nimg = (B + xcds - 1) / xcds;
+    const long full = (nimg * nqb * nqb + slots - 1) / slots;
+    const long sym = (nimg * nqb * (nqb + 1) / 2 + slots - 1) / slots;
+    return 5 * sym < 4 * full;
+}
+
+hipError_t affinity_schedule(int B, int N, int D, int dt, int* schedule)
+{
+    *schedule = kScheduleFull;
+    if (!use_persistent(D, dt)) return hipSuccess;  // the staged kernel covers every pair
+    const int cus = device_cus();
+    if (cus <= 0) return hipErrorInvalidDevice;
+    const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
+    if (symmetric_schedule(B, N, xcds, cus * kPWGS / xcds)) *schedule = kScheduleSymmetric;
+    return hipSuccess;
+}
+
 hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, int D, int dt, float* pv, int32_t* pi,
                            hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
@@ -762,15 +987,22 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
         // workgroups by XCD.
         const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
         const int groups = cus * kPWGS;
-        const int slots = groups / xcds;
-        if (dt == kBf16)
-            hipExtLaunchKernelGGL((affinity_partial_kernel<Bf16, kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES>),
-                                  dim3(groups), dim3(kPWC * kPWQ * kWave), 0, stream, start, stop, 0,
-                                  static_cast<const uint8_t*>(x), x_off, B, N, D, T, xcds, slots, pv, pi);
-        else
-            hipExtLaunchKernelGGL((affinity_partial_kernel<F32, kPWC, kPWQ, kPMT, kPNT, kPCB, kPSTAGES>),
-                                  dim3(groups), dim3(kPWC * kPWQ * kWave), 0, stream, start, stop, 0,
-                                  static_cast<const uint8_t*>(x), x_off, B, N, D, T, xcds, slots, pv, pi);
+        const bool sym = symmetric_schedule(B, N, xcds, groups / xcds);
+        if (dt == kBf16) {
+            if (sym)
+                launch_persistent<Bf16, kSWC, kSWQ, kSMT, kSNT, true>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                                                                       stream, start, stop);
+            else
+                launch_persistent<Bf16, kPWC, kPWQ, kPMT, kPNT, false>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                                                                        stream, start, stop);
+        } else {
+            if (sym)
+                launch_persistent<F32, kSWC, kSWQ, kSMT, kSNT, true>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                                                                      stream, start, stop);
+            else
+                launch_persistent<F32, kPWC, kPWQ, kPMT, kPNT, false>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                                                                       stream, start, stop);
+        }
         return hipGetLastError();
     }
     if (dt == kBf16) return launch_staged<Bf16, 2, 4, 4, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream, start, stop);

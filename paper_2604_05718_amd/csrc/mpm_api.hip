@@ -167,6 +167,19 @@ int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N
                                            static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event)));
 }
 
+int mpm_set_affinity_schedule(int32_t mode) { return mpm::set_affinity_schedule(mode); }
+
+int mpm_affinity_schedule_used(int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* schedule)
+{
+    const int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!schedule) return MPM_ERR_INVALID_ARG;
+    int sc = 0;
+    const int st = hip_status(mpm::affinity_schedule(B, N, D, dt, &sc));
+    if (st == MPM_OK) *schedule = sc;
+    return st;
+}
+
 int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* nb,
                float* best, void* ws, size_t ws_bytes, void* stream)
 {

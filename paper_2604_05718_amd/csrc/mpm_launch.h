@@ -16,6 +16,15 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
 int partial_tiles(int N);
 // Candidate rows covered by one partial of the kernel launch_affinity picks.
 int partial_tile_width(int D, int dt, int N);
+// Work schedule of the persistent affinity kernel: every (query block, candidate
+// tile) pair, only the pairs on and above the diagonal (the symmetric schedule),
+// or a choice by batch shape. Process-wide; returns the previous mode, or -1 (and
+// changes nothing) for an unknown mode.
+enum AffinitySchedule : int { kScheduleAuto = 0, kScheduleFull = 1, kScheduleSymmetric = 2 };
+int set_affinity_schedule(int mode);
+// The schedule (kScheduleFull or kScheduleSymmetric) launch_affinity would run
+// for this shape on the current device under the current mode.
+hipError_t affinity_schedule(int B, int N, int D, int dt, int* schedule);
 hipError_t launch_reduce_partials(const float* pv, const int32_t* pi, const void* x, const int32_t* x_off, int B,
                                   int N, int D, int dt, int32_t* nb, float* best, hipStream_t stream);
 hipError_t launch_pair_compact_partials(const float* pv, const int32_t* pi, int T, int ct, int32_t* nb,

@@ -101,3 +101,29 @@ def test_other_entry_points_reject(lib):
     assert lib.mpm_compose_unmerge(A, None, A, A2, A3, None, 0, 2, 8, 63, 1, A, None) == 1    # D % 8 (bf16)
     assert lib.mpm_compose_unmerge(A, None, A, A2, A3, None, 0, 2, 16385, 64, 1, A, None) == 2
     assert lib.mpm_last_hip_error() == 0
+
+
+def test_affinity_schedule_knob(lib):
+    """Host-only: the schedule setter returns the previous mode, accepts the three
+    mpm_schedule values and rejects anything else without changing the mode."""
+    prev = lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_FULL)
+    try:
+        assert prev in (_lib.MPM_SCHEDULE_AUTO, _lib.MPM_SCHEDULE_FULL, _lib.MPM_SCHEDULE_SYMMETRIC)
+        assert lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_SYMMETRIC) == _lib.MPM_SCHEDULE_FULL
+        for bad in (-1, 3, 1 << 20):
+            assert lib.mpm_set_affinity_schedule(bad) == -1
+        assert lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_AUTO) == _lib.MPM_SCHEDULE_SYMMETRIC
+    finally:
+        lib.mpm_set_affinity_schedule(prev)
+    out = ctypes.c_int32(-7)
+    assert lib.mpm_affinity_schedule_used(0, 1024, 768, 1, ctypes.byref(out)) == _lib.MPM_ERR_INVALID_ARG
+    assert lib.mpm_affinity_schedule_used(64, 1024, 768, 1, None) == _lib.MPM_ERR_INVALID_ARG
+    assert out.value == -7
+    import paper_2604_05718_amd as mpm
+    before = mpm.set_affinity_schedule("full")
+    try:
+        assert mpm.set_affinity_schedule("symmetric") == "full"
+        with pytest.raises(ValueError):
+            mpm.set_affinity_schedule("diagonal")
+    finally:
+        mpm.set_affinity_schedule(before)

@@ -1,6 +1,8 @@
 """Kernel-level parity of the HIP path against the oracle, at small and odd
 shapes that span several tiles and ragged tails (every call goes through the C
 ABI via the ctypes binding)."""
+import zlib
+
 import numpy as np
 import pytest
 import torch
@@ -400,3 +402,115 @@ def test_many_items_per_workgroup():
     torch.cuda.synchronize()
     for b in (0, 7, 8, 23, 39):
         check_schedule_image(x[b], "bf16", res, b)
+
+
+# ---- symmetric affinity schedule ----------------------------------------------
+
+@pytest.fixture
+def schedule(request):
+    prev = mpm.set_affinity_schedule(request.param)
+    yield request.param
+    mpm.set_affinity_schedule(prev)
+
+
+def _affinity_partials(x2, x_off, B, N, D, dtype):
+    """Run mpm_affinity; return the partials (pv, pi) as [B, T, N] host arrays."""
+    from paper_2604_05718_amd import _lib
+    from paper_2604_05718_amd.api import _p, _stream
+    ws = torch.empty((mpm.workspace_bytes(B, N),), dtype=torch.uint8, device=DEV)
+    dt = _lib.MPM_BF16 if dtype == "bf16" else _lib.MPM_F32
+    _lib.check("mpm_affinity", _lib.load().mpm_affinity(_p(x2), _p(x_off), B, N, D, dt, _p(ws), ws.numel(),
+                                                        _stream()))
+    torch.cuda.synchronize()
+    o = _lib.workspace_offsets(B, N)
+    T = (N + 255) // 256
+    pv = ws[o["pv"]:o["pv"] + 4 * B * T * N].view(torch.float32).view(B, T, N).cpu().numpy()
+    pi = ws[o["pi"]:o["pi"] + 4 * B * T * N].view(torch.int32).view(B, T, N).cpu().numpy()
+    return pv, pi
+
+
+def _sym_case(name, dtype):
+    """(rows per image, N, D) of the partial-identity cases."""
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    if name == "dense_777":
+        return [store(clustered(rng, 777, 128, k=30), dtype) for _ in range(3)], 777, 128
+    if name == "duplicated_rows":  # every token twice: exact ties in both directions
+        imgs = []
+        for _ in range(2):
+            h = clustered(rng, 512, 64, k=20)
+            imgs.append(store(np.repeat(h, 2, axis=0), dtype))
+        return imgs, 1024, 64
+    if name == "all_equal":  # every score equal: the lowest index must win everywhere
+        return [store(np.tile(rng.standard_normal((1, 32)), (600, 1)), dtype)], 600, 32
+    if name == "packed_ragged":
+        ns = [1, 256, 257, 512, 513, 1000, 3, 700]
+        return [store(clustered(rng, n, 64, k=25), dtype) for n in ns], 1000, 64
+    raise KeyError(name)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("name", ["dense_777", "duplicated_rows", "all_equal", "packed_ragged"])
+def test_symmetric_schedule_partials_bit_identical(dtype, name):
+    """The symmetric schedule (blocks on and above the diagonal, each off-diagonal
+    block's argmax taken in both directions) must reproduce the full schedule's
+    per-tile partials bit for bit on every valid (token, tile) slot, ties
+    included; its nearest neighbours must then pass the oracle parity check."""
+    rows, N, D = _sym_case(name, dtype)
+    ns = [r.shape[0] for r in rows]
+    B = len(rows)
+    print(f"symmetric partials {name} {dtype} ns={ns} D={D}", flush=True)
+    packed = name == "packed_ragged"
+    if packed:
+        x2 = torch.cat(rows).to(DEV)
+        x_off = torch.from_numpy(np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)).to(DEV)
+    else:
+        x2 = torch.stack(rows).to(DEV).view(B * N, D)
+        x_off = None
+    out = {}
+    for mode in ("full", "symmetric"):
+        prev = mpm.set_affinity_schedule(mode)
+        try:
+            out[mode] = _affinity_partials(x2, x_off, B, N, D, dtype)
+        finally:
+            mpm.set_affinity_schedule(prev)
+    (fv, fi), (sv, si) = out["full"], out["symmetric"]
+    for b, n in enumerate(ns):
+        tiles = (n + 255) // 256
+        assert np.array_equal(fv[b, :tiles, :n].view(np.uint32), sv[b, :tiles, :n].view(np.uint32)), b
+        assert np.array_equal(fi[b, :tiles, :n], si[b, :tiles, :n]), b
+    prev = mpm.set_affinity_schedule("symmetric")
+    try:
+        nb = mpm.argmax(x2 if packed else x2.view(B, N, D), x_off=x_off, N=N if packed else None)
+        torch.cuda.synchronize()
+    finally:
+        mpm.set_affinity_schedule(prev)
+    nb = nb.cpu().numpy()
+    for b, n in enumerate(ns):
+        if n == 1:
+            assert nb[b, 0] == -1
+            continue
+        if name == "all_equal":
+            assert nb[b, 0] == 1 and np.all(nb[b, 1:n] == 0)
+        check_nearest(to64(rows[b]), nb[b, :n])
+
+
+@pytest.mark.parametrize("schedule", ["full", "symmetric"], indirect=True)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_merge_many_tiles_both_schedules(dtype, schedule):
+    """The packed ragged merge with more than four candidate tiles per image,
+    with the affinity schedule forced each way."""
+    rng = np.random.default_rng(43)
+    N, D = 1400, 64
+    ns = [1400, 1311, 1025, 257, 7]
+    rows = [store(clustered(rng, n, D, k=40, sigma=0.3), dtype) for n in ns]
+    off = np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)
+    x = torch.cat(rows).to(DEV)
+    print(f"merge many tiles {dtype} schedule={schedule}", flush=True)
+    res = mpm.merge(x, torch.from_numpy(off).to(DEV), N=N)
+    torch.cuda.synchronize()
+    m = res.map.cpu().numpy()
+    nb = res.nb.cpu().numpy()
+    y = res.y.cpu()
+    y_off = res.y_off.cpu().numpy()
+    for b, n in enumerate(ns):
+        check_stage(to64(rows[b]), dtype, nb[b, :n], m[b], to64(y[y_off[b]:y_off[b + 1]]))
