@@ -364,13 +364,19 @@ __device__ __forceinline__ void exchange_half(float* v, int32_t* ix, int upper)
 // fetched from HBM once and re-read from that XCD's L2 by the other items that
 // use it, instead of being refetched once per candidate tile.
 //
-// Pipeline. The chunks of all the workgroup's items form one stream. Before
-// chunk c is consumed, this wave's loads of chunks up to c+1 have landed and a
-// barrier makes every wave's loads visible and retires the ring slot of chunk
-// c-1, which is then refilled with chunk c+STAGES-1. Within a chunk the MFMA
-// fragments are double-buffered: the fragments of the next k-group (for the
-// last k-group: of the next chunk, already visible) are requested before the
-// current k-group's MFMAs issue, so LDS latency hides behind the matrix cores.
+// Pipeline. The chunks of all the workgroup's items form one stream. With
+// STAGES >= 3, before chunk c is consumed this wave's loads of chunks up to c+1
+// have landed and a barrier makes every wave's loads visible and retires the
+// ring slot of chunk c-1, which is then refilled with chunk c+STAGES-1. Within a
+// chunk the MFMA fragments are double-buffered: the fragments of the next
+// k-group (for the last k-group: of the next chunk, already visible) are
+// requested before the current k-group's MFMAs issue, so LDS latency hides
+// behind the matrix cores. With STAGES == 2 (128-byte chunks: two stages fill
+// 128 KB of LDS) the barrier before chunk c makes chunk c visible and retires
+// chunk c-1's slot; chunk c's first fragments are requested, then chunk c+1's
+// loads into the retired slot, so loads run one chunk ahead. Against 64-byte
+// chunks in four stages this halves the barriers and the load instructions per
+// byte, and each load instruction reads whole 128-byte lines.
 // The global->LDS loads are written as assembly: the compiler cannot tell which
 // ring slot they fill and would otherwise wait for all of them before every LDS
 // read; their completion is waited for explicitly (vmcnt) instead.
@@ -416,7 +422,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     constexpr int STAGE_BYTES = (CT + QT) * CB;
     constexpr int KG = CB / 32;                       // 32-byte k-groups (one MFMA k-step each) per chunk
     static_assert(GROUPS % WAVES == 0 && CT % RPI == 0 && CT % 32 == 0 && QT % 32 == 0, "stage/wave mismatch");
-    static_assert(STAGES >= 3 && (STAGES - 2) * LOADS < 64, "pipeline depth / vmcnt range");
+    static_assert(STAGES >= 2 && (STAGES - 2) * LOADS < 64, "pipeline depth / vmcnt range");
     static_assert(KG % 2 == 0, "the fragment double buffer alternates over an even number of k-groups");
 
     __shared__ __attribute__((aligned(1024))) uint8_t lds[STAGES * STAGE_BYTES];
@@ -508,24 +514,39 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     Offsets ioff = offsets_of(ii);
     int ichunk = 0;
     int issued = 0;
-    auto issue_next = [&]() {
-        if (ii.k >= nitems) return;
-        uint8_t* sb = lds + (issued % STAGES) * STAGE_BYTES;
-        const uint8_t* base = x + (long)ii.row0 * rowbytes + (long)ichunk * CB;   // uniform
-#pragma unroll
-        for (int i = 0; i < LOADS; ++i) {
-            const uint32_t off = ioff.v[i];
-            const uint32_t m0 =
-                (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)(sb + (wave + WAVES * i) * RPI * CB);
-            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(off), "s"(base)
-                         : "memory", "m0");
-        }
+    // The loads of a chunk are issued one at a time between the MFMAs of the chunk before
+    // (issue_part, from mma_issue). Issued together after the barrier, a chunk's loads filled
+    // the load queue and the wave stalled at issue with its MFMAs waiting behind them.
+    uint8_t* isb = lds;
+    const uint8_t* ibase = x;
+    bool iact = false;
+    auto issue_begin = [&]() {
+        iact = ii.k < nitems;
+        isb = lds + (issued % STAGES) * STAGE_BYTES;
+        ibase = x + (long)ii.row0 * rowbytes + (long)ichunk * CB;   // uniform
+    };
+    auto issue_part = [&](int i) {
+        if (!iact) return;
+        const uint32_t off = ioff.v[i];
+        const uint32_t m0 =
+            (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)(isb + (wave + WAVES * i) * RPI * CB);
+        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(off), "s"(ibase)
+                     : "memory", "m0");
+    };
+    auto issue_end = [&]() {
+        if (!iact) return;
         ++issued;
         if (++ichunk == nchunks) {
             ichunk = 0;
             ii = find(ii.k + slots);
             if (ii.k < nitems) ioff = offsets_of(ii);
         }
+    };
+    auto issue_next = [&]() {
+        issue_begin();
+#pragma unroll
+        for (int i = 0; i < LOADS; ++i) issue_part(i);
+        issue_end();
     };
 
     // Row lrow of every 32-row fragment has the same swizzle (32 is a multiple of 16).
@@ -553,15 +574,25 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     float sq[NT];  // query norms (symmetric schedule only)
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) sq[nt] = 0.0f;
-    auto mma = [&](const u32x4 (&fa)[MT], const u32x4 (&fq)[NT]) {
+    // One load part before every PSTEP-th MFMA of a chunk: spread over all of the chunk's MFMAs
+    // with STAGES >= 3, over the first half with two stages (those loads must land before the
+    // chunk ends).
+    constexpr int PGROUPS = KG * MT * NT;  // MFMAs per chunk
+    constexpr int PSPAN = STAGES >= 3 ? PGROUPS : PGROUPS / 2;
+    static_assert(PSPAN >= LOADS && PSPAN % LOADS == 0, "load parts per MFMA");
+    constexpr int PSTEP = PSPAN / LOADS;
+    auto mma_issue = [&](const u32x4 (&fa)[MT], const u32x4 (&fq)[NT], int g) {
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) Mfma<S>::mma(acc[mt][nt], fa[mt], fq[nt]);
-        // Candidate norms: m-tile mt is summed by the wave with wq == mt % WQ only.
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+            for (int nt = 0; nt < NT; ++nt) {
+                const int p = (g * MT + mt) * NT + nt;
+                if (p % PSTEP == 0 && p / PSTEP < LOADS) issue_part(p / PSTEP);
+                Mfma<S>::mma(acc[mt][nt], fa[mt], fq[nt]);
+            }
+            // Candidate norms: m-tile mt is summed by the wave with wq == mt % WQ only.
             if (mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(fa[mt], ss[mt]);
+        }
         if constexpr (SYM) {
             // Query norms, for the reverse direction: n-tile nt is summed by the wave with wc == nt % WC.
 #pragma unroll
@@ -572,39 +603,54 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     // vmcnt(n) with expcnt and lgkmcnt unconstrained.
     constexpr int kWaitAhead = 0x0F70 | ((((STAGES - 2) * LOADS) & 15)) | ((((STAGES - 2) * LOADS) >> 4) << 14);
 
-    // Prologue: STAGES-1 chunks requested, chunk 0 landed and visible, its first fragments requested.
+    // Prologue: STAGES-1 chunks requested; with STAGES >= 3 chunk 0 has also landed, is
+    // visible and has its first fragments requested (with two stages the loop does that).
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s) issue_next();
-    if (issued == STAGES - 1) __builtin_amdgcn_s_waitcnt(kWaitAhead);
-    else __builtin_amdgcn_s_waitcnt(0x0F70);
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    read_frags(fa0, fq0, 0, 0);
+    if constexpr (STAGES >= 3) {
+        if (issued == STAGES - 1) __builtin_amdgcn_s_waitcnt(kWaitAhead);
+        else __builtin_amdgcn_s_waitcnt(0x0F70);
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        read_frags(fa0, fq0, 0, 0);
+    }
 
     Item ci = find(slot);  // compute cursor
     int cchunk = 0;
     int consumed = 0;
     while (ci.k < nitems) {
-        // This wave's loads of chunks up to c+1 have landed (later ones may stay in flight) ...
-        const int ahead = issued - consumed - 2;
-        if (ahead >= STAGES - 2) __builtin_amdgcn_s_waitcnt(kWaitAhead);
-        else if (STAGES > 3 && ahead == 1) __builtin_amdgcn_s_waitcnt(0x0F70 | (LOADS & 15) | ((LOADS >> 4) << 14));
-        else __builtin_amdgcn_s_waitcnt(0x0F70);
-        // ... every wave's are visible, and every wave is done with chunk c-1's slot.
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        issue_next();
+        if constexpr (STAGES >= 3) {
+            // This wave's loads of chunks up to c+1 have landed (later ones may stay in flight) ...
+            const int ahead = issued - consumed - 2;
+            if (ahead >= STAGES - 2) __builtin_amdgcn_s_waitcnt(kWaitAhead);
+            else if (STAGES > 3 && ahead == 1)
+                __builtin_amdgcn_s_waitcnt(0x0F70 | (LOADS & 15) | ((LOADS >> 4) << 14));
+            else __builtin_amdgcn_s_waitcnt(0x0F70);
+            // ... every wave's are visible, and every wave is done with chunk c-1's slot.
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            issue_begin();
+        } else {
+            // Chunk c has landed for this wave; after the barrier for every wave, and every
+            // wave is done with chunk c-1, whose slot then takes chunk c+1.
+            __builtin_amdgcn_s_waitcnt(0x0F70);
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            read_frags(fa0, fq0, consumed, 0);
+            issue_begin();
+        }
 #pragma unroll
         for (int g = 0; g < KG; ++g) {
             if (g + 1 < KG) {
                 if ((g & 1) == 0) read_frags(fa1, fq1, consumed, g + 1);
                 else read_frags(fa0, fq0, consumed, g + 1);
-            } else if (issued > consumed + 1) {
+            } else if (STAGES >= 3 && issued > consumed + 1) {
                 read_frags(fa0, fq0, consumed + 1, 0);
             }
-            if ((g & 1) == 0) mma(fa0, fq0);
-            else mma(fa1, fq1);
+            if ((g & 1) == 0) mma_issue(fa0, fq0, g);
+            else mma_issue(fa1, fq1, g);
         }
+        issue_end();
         ++consumed;
         if (++cchunk < nchunks) continue;
 
@@ -892,13 +938,17 @@ __global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __res
     }
 }
 
-// Persistent-kernel shape: 256 candidates x 256 queries on 8 waves, 64-byte K
-// chunks in a 4-deep ring (128 KB of LDS), one workgroup per CU. The full
+// Persistent-kernel shape: 256 candidates x 256 queries on 8 waves, 128-byte K
+// chunks in a 2-deep ring (or 64-byte chunks 4 deep; 128 KB of LDS either way),
+// one workgroup per CU. The full
 // schedule splits the tile over 2 candidate x 4 query waves (128 x 64 each); the
 // symmetric one over 4 x 2 (64 x 128 each), so that its reverse direction merges 4
 // queries inside each lane before the cross-lane steps and carries half as many
 // rows through them.
-constexpr int kPWC = 2, kPWQ = 4, kPMT = 4, kPNT = 2, kPCB = 64, kPSTAGES = 4, kPWGS = 1;
+constexpr int kPWC = 2, kPWQ = 4, kPMT = 4, kPNT = 2, kPCB = 64, kPWGS = 1;
+// Rows that are a whole number of 128-byte chunks stream them through two stages;
+// other multiples of 64 bytes use 64-byte chunks in four stages.
+constexpr int kPCB2 = 128;
 constexpr int kSWC = 4, kSWQ = 2, kSMT = 2, kSNT = 4;
 constexpr int kPCT = kPWC * kPMT * 32;
 static_assert(kSWC * kSMT * 32 == kPCT && kSWQ * kSNT * 32 == kPCT && kPWQ * kPNT * 32 == kPCT,
@@ -920,9 +970,15 @@ template <class S, int WC, int WQ, int MT, int NT, bool SYM>
 void launch_persistent(const void* x, const int32_t* x_off, int B, int N, int D, int T, int xcds, int groups,
                        float* pv, int32_t* pi, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
-    hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB, kPSTAGES, SYM>), dim3(groups),
-                          dim3(WC * WQ * kWave), 0, stream, start, stop, 0, static_cast<const uint8_t*>(x), x_off, B,
-                          N, D, T, xcds, groups / xcds, pv, pi);
+    const uint8_t* xb = static_cast<const uint8_t*>(x);
+    if (((long)D * S::kBytes) % kPCB2 == 0)
+        hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB2, 2, SYM>), dim3(groups),
+                              dim3(WC * WQ * kWave), 0, stream, start, stop, 0, xb, x_off, B, N, D, T, xcds,
+                              groups / xcds, pv, pi);
+    else
+        hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB, 4, SYM>), dim3(groups),
+                              dim3(WC * WQ * kWave), 0, stream, start, stop, 0, xb, x_off, B, N, D, T, xcds,
+                              groups / xcds, pv, pi);
 }
 
 template <class S, int WC, int WQ, int MT, int NT, int CHUNK>

@@ -434,6 +434,8 @@ def _sym_case(name, dtype):
     rng = np.random.default_rng(zlib.crc32(name.encode()))
     if name == "dense_777":
         return [store(clustered(rng, 777, 128, k=30), dtype) for _ in range(3)], 777, 128
+    if name == "rows_192_bytes":  # bf16 rows of 192 bytes: the 64-byte-chunk, four-stage pipeline
+        return [store(clustered(rng, 777, 96, k=30), dtype) for _ in range(3)], 777, 96
     if name == "duplicated_rows":  # every token twice: exact ties in both directions
         imgs = []
         for _ in range(2):
@@ -449,7 +451,7 @@ def _sym_case(name, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("name", ["dense_777", "duplicated_rows", "all_equal", "packed_ragged"])
+@pytest.mark.parametrize("name", ["dense_777", "rows_192_bytes", "duplicated_rows", "all_equal", "packed_ragged"])
 def test_symmetric_schedule_partials_bit_identical(dtype, name):
     """The symmetric schedule (blocks on and above the diagonal, each off-diagonal
     block's argmax taken in both directions) must reproduce the full schedule's
