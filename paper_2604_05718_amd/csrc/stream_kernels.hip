@@ -2,10 +2,12 @@
 // composition (Eq. 3) and gather reconstruction (Eq. 4).
 //
 // The row kernels treat a token row as D*s/16 independent 16-byte vectors and
-// give every lane one vector at a time, so any D keeps all lanes busy and
-// every global access is a 16-byte, fully coalesced load or store. Output rows
-// are written once and never re-read by the kernel, so they are stored with
-// non-temporal hints.
+// deal them to the lanes with the workgroup size as stride, so any D keeps all
+// lanes busy and every global access is a 16-byte, fully coalesced load or
+// store. A lane loads a small batch of vectors before storing any, so several
+// loads per lane are in flight (one load then one store per lane left the
+// gather latency-bound). Output rows are written once and never re-read by the
+// kernel, so they are stored with non-temporal hints.
 #include "mpm_device.h"
 #include "mpm_launch.h"
 
@@ -15,13 +17,17 @@ namespace {
 constexpr int kRowThreads = 256;
 constexpr int kRowBytesPerBlock = 32768;     // output bytes one workgroup handles
 constexpr int kGatherBytesPerBlock = 16384;  // ... in the gather, which first resolves its rows' sources
+// Vectors each thread loads before storing them (loads in flight per thread).
+constexpr int kGatherBatch = 4;
+constexpr int kAverageBatch = 2;  // each vector of the average already loads two rows
 constexpr int kMaxRowsPerBlock = 4096;       // rows one gather workgroup resolves into LDS (16 KB)
 
-// Walks the flat range [f0, f1) of 16-byte vectors of a row-major block whose
-// rows hold `vpr` vectors, calling body(row, vec) with a stride of the
-// workgroup size; row/column advance incrementally (no per-element division).
-template <class Body>
-__device__ __forceinline__ void for_each_vec(long f0, long f1, int vpr, Body body)
+// Walks the flat range [f0, f1) of 16-byte vectors of a row-major block whose rows
+// hold `vpr` vectors, U vectors per lane at a time (stride of the workgroup size):
+// load(row, vec) for all U, then store(row, vec, value) for all U. Row and column
+// advance incrementally (no per-element division).
+template <int U, class Load, class Store>
+__device__ __forceinline__ void for_each_vec_batched(long f0, long f1, int vpr, Load load, Store store)
 {
     const int t = threadIdx.x;
     long f = f0 + t;
@@ -30,14 +36,28 @@ __device__ __forceinline__ void for_each_vec(long f0, long f1, int vpr, Body bod
     int col = (int)(f - row * vpr);
     const int step_rows = kRowThreads / vpr;
     const int step_cols = kRowThreads - step_rows * vpr;
-    for (; f < f1; f += kRowThreads) {
-        body(row, col);
-        row += step_rows;
-        col += step_cols;
-        if (col >= vpr) {
-            col -= vpr;
-            row += 1;
+    while (f < f1) {
+        u32x4 v[U];
+        long rr[U];
+        int cc[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            ok[u] = f < f1;
+            rr[u] = row;
+            cc[u] = col;
+            if (ok[u]) v[u] = load(row, col);
+            f += kRowThreads;
+            row += step_rows;
+            col += step_cols;
+            if (col >= vpr) {
+                col -= vpr;
+                row += 1;
+            }
         }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) store(rr[u], cc[u], v[u]);
     }
 }
 
@@ -76,14 +96,16 @@ __global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
     const uint8_t* ximg = x + (long)(x_off ? x_off[b] : b * N) * rowbytes;
     uint8_t* yimg = y + (long)off * rowbytes;
     const int32_t* srcb = src + 2L * b * N;
-    for_each_vec((long)k0 * vpr, (long)k1 * vpr, vpr, [&](long k, int c) {
-        const int ia = srcb[2 * k];
-        const int ib = srcb[2 * k + 1];
-        const u32x4 va = load16(ximg + ia * rowbytes + c * 16);
-        u32x4 out = va;  // a singleton is copied bit for bit
-        if (ib != ia) out = mean16(va, load16(ximg + ib * rowbytes + c * 16), S{});
-        store16_stream(yimg + k * rowbytes + c * 16, out);
-    });
+    for_each_vec_batched<kAverageBatch>((long)k0 * vpr, (long)k1 * vpr, vpr,
+        [&](long k, int c) {
+            const int ia = srcb[2 * k];
+            const int ib = srcb[2 * k + 1];
+            const u32x4 va = load16(ximg + ia * rowbytes + c * 16);
+            u32x4 out = va;  // a singleton is copied bit for bit
+            if (ib != ia) out = mean16(va, load16(ximg + ib * rowbytes + c * 16), S{});
+            return out;
+        },
+        [&](long k, int c, u32x4 out) { store16_stream(yimg + k * rowbytes + c * 16, out); });
 }
 
 __global__ __launch_bounds__(kRowThreads) void compose_kernel(const int32_t* map_a,
@@ -132,16 +154,18 @@ __global__ __launch_bounds__(kRowThreads) void unmerge_kernel(
         src_row[r - r0] = m;
     }
     __syncthreads();
-    for_each_vec((long)r0 * vpr, (long)r1 * vpr, vpr, [&](long r, int c) {
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (r < E) {
-            v = load16(z_spec + ((long)b * E + r) * rowbytes + c * 16);
-        } else {
-            const int m = src_row[r - r0];
-            if (m >= 0) v = load16(zimg + m * rowbytes + c * 16);
-        }
-        store16_stream(oimg + r * rowbytes + c * 16, v);
-    });
+    for_each_vec_batched<kGatherBatch>((long)r0 * vpr, (long)r1 * vpr, vpr,
+        [&](long r, int c) {
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (r < E) {
+                v = load16(z_spec + ((long)b * E + r) * rowbytes + c * 16);
+            } else {
+                const int m = src_row[r - r0];
+                if (m >= 0) v = load16(zimg + m * rowbytes + c * 16);
+            }
+            return v;
+        },
+        [&](long r, int c, u32x4 v) { store16_stream(oimg + r * rowbytes + c * 16, v); });
 }
 
 int rows_per_block_for(long rowbytes, long block_bytes = kRowBytesPerBlock)
