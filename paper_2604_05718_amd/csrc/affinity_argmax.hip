@@ -358,13 +358,11 @@ __device__ __forceinline__ void exchange_half(float* v, int32_t* ix, int upper)
 //
 // Scheduling for the 8 per-XCD L2 caches: workgroups are dealt round-robin to
 // the XCDs, so workgroup w serves XCD group w % xcds; a group owns the images
-// b = group + xcds * i and its `slots` workgroups take the group's items one
-// round at a time, image by image, so the items running together on an XCD
-// come from a few images and re-read their 256-row blocks from that XCD's L2
-// instead of HBM. The symmetric schedule orders a group's items longest first
-// (off-diagonal items, which also take the reverse direction, then diagonal
-// ones) and alternates the slot order from round to round, so the slots that
-// run one item more take cheaper ones.
+// b = group + xcds * i and its `slots` workgroups take the group's items in
+// order (item k goes to slot k % slots). All items of an image therefore run at
+// the same time on one XCD, in lockstep over K, and each 256-row block is
+// fetched from HBM once and re-read from that XCD's L2 by the other items that
+// use it, instead of being refetched once per candidate tile.
 //
 // Pipeline. The chunks of all the workgroup's items form one stream. With
 // STAGES >= 3, before chunk c is consumed this wave's loads of chunks up to c+1
@@ -457,40 +455,20 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     struct Item {
         int k, b, qbase, cbase, n, row0;
     };
-    // A cursor k = round * slots + slot walks this workgroup's items, one per round;
-    // kDone marks the end. Full schedule: round r of slot s takes item r*slots + s of the
-    // group (image by image, the blocks of an image row by row). Symmetric schedule: the
-    // off-diagonal items (which also take the reverse direction, about a fifth dearer)
-    // come first, image by image, then the diagonal ones, and the rounds alternate the
-    // slot order (snake). Where the items do not divide evenly, the slots that run one
-    // item more then take the cheaper, diagonal ones.
-    constexpr int kDone = 0x3fffffff;
-    const int n_off = nqb * (nqb - 1) / 2;  // off-diagonal items per image
     auto find = [&](int k) {
         Item it;
-        for (;; k += slots) {
-            const int round = k / slots;
-            const int q = round * slots + ((round & 1) && SYM ? slots - 1 - slot : slot);
-            if (q >= nitems) break;
-            int ib, qb, t;
-            if (SYM) {
-                if (q < nimg * n_off) {  // off-diagonal pairs qb < t of an image, row by row
-                    ib = q / n_off;
-                    int w = q - ib * n_off;
-                    qb = 0;
-                    while (w >= nqb - 1 - qb) {
-                        w -= nqb - 1 - qb;
-                        ++qb;
-                    }
-                    t = qb + 1 + w;
-                } else {
-                    const int d = q - nimg * n_off;
-                    ib = d / nqb;
-                    qb = t = d - ib * nqb;
+        for (; k < nitems; k += slots) {
+            const int ib = k / per_img;
+            int w = k - ib * per_img;
+            int qb, t;
+            if (SYM) {  // blocks qb <= t of the upper triangle, row by row
+                qb = 0;
+                while (w >= nqb - qb) {
+                    w -= nqb - qb;
+                    ++qb;
                 }
+                t = qb + w;
             } else {
-                ib = q / per_img;
-                const int w = q - ib * per_img;
                 qb = w / T;
                 t = w - qb * T;
             }
@@ -502,7 +480,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                 return it;
             }
         }
-        it.k = kDone; it.b = 0; it.qbase = 0; it.cbase = 0; it.n = 1; it.row0 = 0;
+        it.k = nitems; it.b = 0; it.qbase = 0; it.cbase = 0; it.n = 1; it.row0 = 0;
         return it;
     };
 
@@ -543,7 +521,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     const uint8_t* ibase = x;
     bool iact = false;
     auto issue_begin = [&]() {
-        iact = ii.k < kDone;
+        iact = ii.k < nitems;
         isb = lds + (issued % STAGES) * STAGE_BYTES;
         ibase = x + (long)ii.row0 * rowbytes + (long)ichunk * CB;   // uniform
     };
@@ -561,7 +539,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         if (++ichunk == nchunks) {
             ichunk = 0;
             ii = find(ii.k + slots);
-            if (ii.k < kDone) ioff = offsets_of(ii);
+            if (ii.k < nitems) ioff = offsets_of(ii);
         }
     };
     auto issue_next = [&]() {
@@ -640,7 +618,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     Item ci = find(slot);  // compute cursor
     int cchunk = 0;
     int consumed = 0;
-    while (ci.k < kDone) {
+    while (ci.k < nitems) {
         if constexpr (STAGES >= 3) {
             // This wave's loads of chunks up to c+1 have landed (later ones may stay in flight) ...
             const int ahead = issued - consumed - 2;
