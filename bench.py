@@ -32,8 +32,8 @@ AFF_SAMPLE = 8   # every 8th timed step carries the affinity kernels' timing eve
 # HBM traffic of the affinity-argmax kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "2b4e2dfffee0079b76fea8ed3e13d53a5fbce9aa1558e6eab96b06fe50a5f0ca",
-           "bytes_per_launch": 106196464}
+TRAFFIC = {"source_sha256": "bc572f5770bd771e3943ca8d123049971a244d4f5961000773c44750d142fcfd",
+           "bytes_per_launch": 107434003}
 
 
 def log(*a):
