@@ -80,7 +80,6 @@ def algorithmic_work(cfg, counts):
     # gather: read the composed map, each final row once, write the full grid
     gather = sum(4.0 * N + m * D * s + N * D * s for m in n_in)
     if cfg.insertions == 1:
-        work.append(("bytes", 8.0 * N * B))
         work.append(("bytes", gather))
         return work
     # compose: read r* (4N), touch the stage map of the previous survivors (4 n), write r* (4N);

@@ -254,7 +254,8 @@ class Schedule:
         self.map = [torch.empty((B, N), **i32) for _ in range(insertions)]
         self.y = [torch.empty((B * N, D), dtype=dtype, device=dev) for _ in range(insertions)]
         self.y_off = [torch.empty((B + 1,), **i32) for _ in range(insertions)]
-        self.rstar = torch.empty((B, N), **i32)
+        # With one insertion the map is the composed map: the gather reads it directly.
+        self.rstar = self.map[0] if insertions == 1 else torch.empty((B, N), **i32)
         self.rchain = torch.empty((B, N), **i32) if insertions > 2 else None  # maps composed before the last
         self.out = torch.empty((B, N, D), dtype=dtype, device=dev)
         self._lib = _lib.load()
@@ -266,7 +267,7 @@ class Schedule:
         for s in range(self.insertions):
             names += [f"affinity{s + 1}", f"compact{s + 1}", f"average{s + 1}"]
         if self.insertions == 1:
-            return names + ["copy_map", "unmerge"]
+            return names + ["unmerge"]
         # the last composition runs inside the gather (mpm_compose_unmerge)
         return names + ["compose"] * (self.insertions - 2) + ["compose+unmerge"]
 
@@ -305,8 +306,6 @@ class Schedule:
                                                                 _p(self.y_off[s]), st))
             cur, cur_off = self.y[s], self.y_off[s]
         if self.insertions == 1:
-            mark()
-            self.rstar.copy_(self.map[0])
             mark()
             _lib.check("mpm_unmerge", lib.mpm_unmerge(_p(cur), _p(cur_off), _p(self.rstar), None, 0, B, N, D, dt,
                                                       _p(self.out), st))

@@ -898,46 +898,6 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     }
 }
 
-// nb[b*N + i] = lexicographic max over the candidate-tile partials of row i
-// (larger score, then smaller index); optional cosine of the chosen pair.
-template <class S>
-__global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __restrict__ pv,
-                                                               const int32_t* __restrict__ pi,
-                                                               const uint8_t* __restrict__ x,
-                                                               const int32_t* __restrict__ x_off, int B, int N,
-                                                               int D, int T, int ct, int32_t* __restrict__ nb,
-                                                               float* __restrict__ best)
-{
-    const long g = (long)blockIdx.x * 256 + threadIdx.x;
-    if (g >= (long)B * N) return;
-    const int b = (int)(g / N);
-    const int i = (int)(g - (long)b * N);
-    const int row0 = x_off ? x_off[b] : b * N;
-    const int n = x_off ? x_off[b + 1] - row0 : N;
-    if (i >= n) return;
-    const int tiles = (n + ct - 1) / ct;
-    float v = -__builtin_inff();
-    int32_t j = -1;
-    for (int t = 0; t < tiles; ++t) {
-        const long o = ((long)b * T + t) * N + i;
-        const float ov = pv[o];
-        const int32_t oi = pi[o];
-        if (ov > v || (ov == v && (uint32_t)oi < (uint32_t)j)) {
-            v = ov;
-            j = oi;
-        }
-    }
-    nb[g] = j;
-    if (best) {
-        // Diagnostic only: divide by the query's own norm to report the cosine.
-        const long rowbytes = (long)D * S::kBytes;
-        const uint8_t* xr = x + ((long)row0 + i) * rowbytes;
-        float t2 = 0.0f;
-        for (long kk = 0; kk < rowbytes; kk += 16) t2 = Mfma<S>::sumsq(load16(xr + kk), t2);
-        best[g] = j >= 0 ? v / fmaxf(sqrtf(t2), 1e-12f) : -__builtin_inff();
-    }
-}
-
 // Persistent-kernel shape: 256 candidates x 256 queries on 8 waves, 128-byte K
 // chunks in a 2-deep ring (or 64-byte chunks 4 deep; 128 KB of LDS either way),
 // one workgroup per CU. The full
@@ -1063,23 +1023,6 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
     }
     if (dt == kBf16) return launch_staged<Bf16, 2, 4, 4, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream, start, stop);
     return launch_staged<F32, 2, 2, 2, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream, start, stop);
-}
-
-hipError_t launch_reduce_partials(const float* pv, const int32_t* pi, const void* x, const int32_t* x_off, int B,
-                                  int N, int D, int dt, int32_t* nb, float* best, hipStream_t stream)
-{
-    const int T = partial_tiles(N);
-    const int ct = partial_tile_width(D, dt, N);
-    const long total = (long)B * N;
-    const dim3 grid((unsigned)((total + 255) / 256));
-    const uint8_t* xp = static_cast<const uint8_t*>(x);
-    if (dt == kBf16)
-        hipLaunchKernelGGL(reduce_partials_kernel<Bf16>, grid, dim3(256), 0, stream, pv, pi, xp, x_off, B, N, D, T, ct,
-                           nb, best);
-    else
-        hipLaunchKernelGGL(reduce_partials_kernel<F32>, grid, dim3(256), 0, stream, pv, pi, xp, x_off, B, N, D, T, ct,
-                           nb, best);
-    return hipGetLastError();
 }
 
 }  // namespace mpm

@@ -1,13 +1,13 @@
 // Mutual-pair test, RepMask and compact ids (Sec. 3.2, Alg. 1) for gfx950.
 //
-// One workgroup of 1024 threads per image. Tokens are visited in rounds of
-// 1024; in each round every thread decides whether its token is a
-// representative (not in a mutual pair, or the lower index of one), the wave
-// ballots the flags and each lane's rank inside the wave is the popcount of
-// the ballot below it; wave totals are scanned through LDS. A running base
-// carries the count across rounds, so ids follow the left-to-right scan of
-// the paper. Neighbours and representative ids are kept in LDS, and partners
-// then copy the id of their (lower-index) representative.
+// One workgroup of 1024 threads per image. The neighbours of the image are
+// gathered into LDS (reduced from the affinity kernel's per-tile partials, or
+// read from nb). Each thread then takes a contiguous run of ceil(n/1024)
+// tokens, counts the representatives in it (not in a mutual pair, or the lower
+// index of one), and one workgroup-wide exclusive scan of the counts gives the
+// id of the run's first representative, so ids follow the left-to-right scan
+// of the paper. Partners then copy the id of their (lower-index)
+// representative.
 #include "mpm_device.h"
 #include "mpm_launch.h"
 
@@ -16,10 +16,36 @@ namespace {
 
 constexpr int kCompactThreads = 1024;
 constexpr int kCompactWaves = kCompactThreads / kWave;
+constexpr int kPartialBatch = 4;  // partial tiles whose loads are issued together
 
 __device__ __forceinline__ bool is_mutual(const int32_t* nbl, int i, int j, int n)
 {
     return j >= 0 && j < n && j != i && nbl[j] == i;
+}
+
+// Exclusive prefix sum of one value per thread over the workgroup (wave scans
+// by lane shuffles, wave totals through LDS); *total receives the sum.
+__device__ __forceinline__ int block_exclusive_scan(int v, int32_t* wave_sum, int* total)
+{
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        x += lane >= o ? y : 0;
+    }
+    if (lane == kWave - 1) wave_sum[wave] = x;
+    __syncthreads();
+    int before = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kCompactWaves; ++w) {
+        const int c = wave_sum[w];
+        before += w < wave ? c : 0;
+        all += c;
+    }
+    *total = all;
+    return before + x - v;
 }
 
 // FROM_PARTIALS: nb is first reduced from the affinity kernel's per-tile
@@ -34,27 +60,32 @@ __global__ __launch_bounds__(kCompactThreads) void pair_compact_kernel(
     extern __shared__ int32_t lds[];
     int32_t* nbl = lds;       // nearest neighbour per token, N entries
     int32_t* rid = lds + N;   // compact id per representative, N entries
-    __shared__ int32_t wave_total[kCompactWaves];
+    __shared__ int32_t wave_sum[kCompactWaves];
 
     const int b = blockIdx.x;
     const int n = x_off ? x_off[b + 1] - x_off[b] : N;
     const int tid = threadIdx.x;
-    const int lane = tid & (kWave - 1);
-    const int wave = tid / kWave;
-    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
 
     if (FROM_PARTIALS) {
         const int tiles = (n + ct - 1) / ct;
         for (int i = tid; i < n; i += kCompactThreads) {
             float v = -__builtin_inff();
             int32_t j = -1;
-            for (int t = 0; t < tiles; ++t) {
-                const long o = ((long)b * T + t) * N + i;
-                const float ov = pv[o];
-                const int32_t oi = pi[o];
-                if (ov > v || (ov == v && (uint32_t)oi < (uint32_t)j)) {
-                    v = ov;
-                    j = oi;
+            for (int t0 = 0; t0 < tiles; t0 += kPartialBatch) {
+                float ov[kPartialBatch];
+                int32_t oi[kPartialBatch];
+#pragma unroll
+                for (int u = 0; u < kPartialBatch; ++u) {
+                    const long o = ((long)b * T + t0 + u) * N + i;
+                    ov[u] = t0 + u < tiles ? pv[o] : -__builtin_inff();
+                    oi[u] = t0 + u < tiles ? pi[o] : -1;
+                }
+#pragma unroll
+                for (int u = 0; u < kPartialBatch; ++u) {
+                    if (ov[u] > v || (ov[u] == v && (uint32_t)oi[u] < (uint32_t)j)) {
+                        v = ov[u];
+                        j = oi[u];
+                    }
                 }
             }
             nbl[i] = j;
@@ -65,47 +96,107 @@ __global__ __launch_bounds__(kCompactThreads) void pair_compact_kernel(
     }
     __syncthreads();
 
-    int base = 0;
-    for (int i0 = 0; i0 < n; i0 += kCompactThreads) {
-        const int i = i0 + tid;
-        int j = -1;
-        bool mutual = false, rep = false;
-        if (i < n) {
-            j = nbl[i];
-            mutual = is_mutual(nbl, i, j, n);
-            rep = !mutual || i < j;
-        }
-        const uint64_t ballot = __ballot(rep);
-        const int rank = __popcll(ballot & below);
-        if (lane == 0) wave_total[wave] = __popcll(ballot);
-        __syncthreads();
-        int before = 0, round_total = 0;
-#pragma unroll
-        for (int w = 0; w < kCompactWaves; ++w) {
-            const int c = wave_total[w];
-            before += (w < wave) ? c : 0;
-            round_total += c;
-        }
-        if (rep) {
-            const int id = base + before + rank;
+    // This thread's run of tokens and the representatives in it.
+    const int per = (n + kCompactThreads - 1) / kCompactThreads;
+    const int i0 = min(n, tid * per);
+    const int i1 = min(n, i0 + per);
+    int reps = 0;
+    for (int i = i0; i < i1; ++i) {
+        const int j = nbl[i];
+        reps += (!is_mutual(nbl, i, j, n) || i < j) ? 1 : 0;
+    }
+    int total;
+    int id = block_exclusive_scan(reps, wave_sum, &total);
+    for (int i = i0; i < i1; ++i) {
+        const int j = nbl[i];
+        const bool mutual = is_mutual(nbl, i, j, n);
+        if (!mutual || i < j) {
             rid[i] = id;
             const long k = (long)b * N + id;
             src[2 * k] = i;
             src[2 * k + 1] = mutual ? j : i;
+            ++id;
         }
-        base += round_total;
-        __syncthreads();  // wave_total is rewritten next round; rid complete after the last
     }
+    __syncthreads();  // rid complete
 
     for (int i = tid; i < N; i += kCompactThreads) {
-        int id = -1;
+        int m = -1;
         if (i < n) {
             const int j = nbl[i];
-            id = (is_mutual(nbl, i, j, n) && j < i) ? rid[j] : rid[i];
+            m = (is_mutual(nbl, i, j, n) && j < i) ? rid[j] : rid[i];
         }
-        map[(long)b * N + i] = id;
+        map[(long)b * N + i] = m;
     }
-    if (tid == 0) count[b] = base;
+    if (tid == 0) count[b] = total;
+}
+
+// Sum of squares of one 16-byte group of storage values, in float32.
+__device__ __forceinline__ float sumsq16(u32x4 a, float s, Bf16)
+{
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        s = fmaf(bf16_lo(a[e]), bf16_lo(a[e]), s);
+        s = fmaf(bf16_hi(a[e]), bf16_hi(a[e]), s);
+    }
+    return s;
+}
+
+__device__ __forceinline__ float sumsq16(u32x4 a, float s, F32)
+{
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s = fmaf(__uint_as_float(a[e]), __uint_as_float(a[e]), s);
+    return s;
+}
+
+// nb[b*N + i] = lexicographic max over the candidate-tile partials of row i
+// (larger score, then smaller index); optional cosine of the chosen pair.
+template <class S>
+__global__ __launch_bounds__(256) void reduce_partials_kernel(const float* __restrict__ pv,
+                                                               const int32_t* __restrict__ pi,
+                                                               const uint8_t* __restrict__ x,
+                                                               const int32_t* __restrict__ x_off, int B, int N,
+                                                               int D, int T, int ct, int32_t* __restrict__ nb,
+                                                               float* __restrict__ best)
+{
+    const long g = (long)blockIdx.x * 256 + threadIdx.x;
+    if (g >= (long)B * N) return;
+    const int b = (int)(g / N);
+    const int i = (int)(g - (long)b * N);
+    const int row0 = x_off ? x_off[b] : b * N;
+    const int n = x_off ? x_off[b + 1] - row0 : N;
+    if (i >= n) return;
+    const int tiles = (n + ct - 1) / ct;
+    float v = -__builtin_inff();
+    int32_t j = -1;
+    // The partials of 8 tiles are loaded before any is merged, so their loads overlap.
+    constexpr int kBatch = 8;
+    for (int t0 = 0; t0 < tiles; t0 += kBatch) {
+        float ov[kBatch];
+        int32_t oi[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const long o = ((long)b * T + t0 + u) * N + i;
+            ov[u] = t0 + u < tiles ? pv[o] : -__builtin_inff();
+            oi[u] = t0 + u < tiles ? pi[o] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (ov[u] > v || (ov[u] == v && (uint32_t)oi[u] < (uint32_t)j)) {
+                v = ov[u];
+                j = oi[u];
+            }
+        }
+    }
+    nb[g] = j;
+    if (best) {
+        // Diagnostic only: divide by the query's own norm to report the cosine.
+        const long rowbytes = (long)D * S::kBytes;
+        const uint8_t* xr = x + ((long)row0 + i) * rowbytes;
+        float t2 = 0.0f;
+        for (long kk = 0; kk < rowbytes; kk += 16) t2 = sumsq16(load16(xr + kk), t2, S{});
+        best[g] = j >= 0 ? v / fmaxf(sqrtf(t2), 1e-12f) : -__builtin_inff();
+    }
 }
 
 template <bool FROM_PARTIALS>
@@ -137,6 +228,23 @@ hipError_t launch_pair_compact_partials(const float* pv, const int32_t* pi, int 
                                         int32_t* count, hipStream_t stream)
 {
     return launch_compact_t<true>(pv, pi, T, ct, nb, x_off, B, N, map, src, count, stream);
+}
+
+hipError_t launch_reduce_partials(const float* pv, const int32_t* pi, const void* x, const int32_t* x_off, int B,
+                                  int N, int D, int dt, int32_t* nb, float* best, hipStream_t stream)
+{
+    const int T = partial_tiles(N);
+    const int ct = partial_tile_width(D, dt, N);
+    const long total = (long)B * N;
+    const dim3 grid((unsigned)((total + 255) / 256));
+    const uint8_t* xp = static_cast<const uint8_t*>(x);
+    if (dt == kBf16)
+        hipLaunchKernelGGL(reduce_partials_kernel<Bf16>, grid, dim3(256), 0, stream, pv, pi, xp, x_off, B, N, D, T, ct,
+                           nb, best);
+    else
+        hipLaunchKernelGGL(reduce_partials_kernel<F32>, grid, dim3(256), 0, stream, pv, pi, xp, x_off, B, N, D, T, ct,
+                           nb, best);
+    return hipGetLastError();
 }
 
 }  // namespace mpm
