@@ -47,17 +47,19 @@ def kernel_source_hash() -> str:
 
 
 def executed_affinity_flops(cfg, counts, schedule):
-    """Matrix-core flops each affinity launch issues: 2 * 256^2 * D per 256 x 256
-    block, nb^2 blocks per image of nb = ceil(n / 256) blocks under the full
-    schedule, nb (nb + 1) / 2 under the symmetric one (padding rows included)."""
+    """Matrix-core flops each affinity launch issues: 2 * w^2 * D per w x w block,
+    nb^2 blocks per image of nb = ceil(n / w) blocks under the full schedules
+    (w = 256, or 64 for full_64), nb (nb + 1) / 2 under the symmetric one
+    (padding rows included)."""
+    w = 64 if schedule == "full_64" else 256
     out = []
     n_in = [cfg.N] * cfg.B
     for st in range(cfg.insertions):
         blocks = 0
         for n in n_in:
-            nb = (n + 255) // 256
+            nb = (n + w - 1) // w
             blocks += nb * (nb + 1) // 2 if schedule == "symmetric" else nb * nb
-        out.append(blocks * 2.0 * 256 * 256 * cfg.D)
+        out.append(blocks * 2.0 * w * w * cfg.D)
         n_in = counts[st]
     return out
 

@@ -69,9 +69,11 @@ typedef enum {
 } mpm_dtype;
 
 typedef enum {
-    MPM_SCHEDULE_AUTO = 0,      /* symmetric when it needs fewer work rounds (default) */
+    MPM_SCHEDULE_AUTO = 0,      /* 64 x 64 blocks for small batches, else symmetric when it
+                                   needs fewer work rounds (default) */
     MPM_SCHEDULE_FULL = 1,      /* every (query block, candidate tile) pair */
-    MPM_SCHEDULE_SYMMETRIC = 2  /* pairs on and above the block diagonal only */
+    MPM_SCHEDULE_SYMMETRIC = 2, /* pairs on and above the block diagonal only */
+    MPM_SCHEDULE_FULL_64 = 3    /* every pair of 64 x 64 blocks (small batches) */
 } mpm_schedule;
 
 #define MPM_MAX_N 16384   /* tokens per image */
@@ -97,7 +99,10 @@ int mpm_last_hip_error(void);
  *   src   int32[2*B*N]        (representative, partner) per cluster;
  *   count int32[B]            clusters per image;
  *   pv    float[B*T*N], pi int32[B*T*N]  per-candidate-tile argmax partials,
- *                             T = ceil(N / 256).
+ *                             T = ceil(N / 64) slots per token: tile t of image b
+ *                             for token i at (b*T + t)*N + i; a launch fills the
+ *                             first ceil(n_b / w) slots, w = the block width of
+ *                             its schedule (64 or 256 tokens).
  * Returns 0 for B < 1 or N < 1.
  */
 size_t mpm_workspace_bytes(int32_t B, int32_t N);
@@ -135,29 +140,35 @@ int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N
 
 /*
  * Work schedule of the affinity kernel, for tuning and testing; results do not
- * depend on it (the partials are bit-identical). The affinity of an image is
- * symmetric (Eq. 1), so the symmetric schedule computes only the 256 x 256
- * blocks on and above the block diagonal and takes each off-diagonal block's
- * argmax in both directions, about half the matrix-core work for large images
- * at the price of a cross-lane reduction per block. MPM_SCHEDULE_AUTO (the
- * default) picks it when it needs fewer work rounds on the device's compute
- * units. Applies to bfloat16 and float32 rows whose byte length is a multiple
- * of 64 (other rows use a kernel without a schedule choice). Process-wide: it
- * affects every later call on any thread; calls already enqueued are not
- * changed. Returns the previous mode, or -1 (changing nothing) when `mode` is
- * not an mpm_schedule value.
+ * depend on it (the partials are bit-identical, and so are the nearest
+ * neighbours reduced from them). The affinity of an image is symmetric
+ * (Eq. 1), so the symmetric schedule computes only the 256 x 256 blocks on and
+ * above the block diagonal and takes each off-diagonal block's argmax in both
+ * directions, about half the matrix-core work for large images at the price of
+ * a cross-lane reduction per block. MPM_SCHEDULE_FULL_64 computes every pair of
+ * 64 x 64 blocks, so that a small batch (a single image of 1024 tokens has 16
+ * blocks of 256 x 256 but 256 of 64 x 64) still occupies every compute unit.
+ * MPM_SCHEDULE_AUTO (the default) takes the 64 x 64 blocks when the batch has
+ * at most 32 blocks of 256 x 256, else the symmetric schedule when it needs
+ * fewer work rounds on the device's compute units, else the full one. Applies
+ * to bfloat16 and float32 rows whose byte length is a multiple of 64 (other
+ * rows use a kernel without a schedule choice). Process-wide: it affects every
+ * later call on any thread; calls already enqueued are not changed. Returns the
+ * previous mode, or -1 (changing nothing) when `mode` is not an mpm_schedule
+ * value.
  */
 int mpm_set_affinity_schedule(int32_t mode);
 
 /*
- * The schedule (MPM_SCHEDULE_FULL or MPM_SCHEDULE_SYMMETRIC, never AUTO) that
- * mpm_affinity would run for B images of at most N tokens of D channels of
- * dtype dt on the current device under the current mode, written to
- * *schedule (a host pointer). For reporting the matrix-core work a call
- * issues: about 2 * 256^2 * D flops per 256 x 256 block, nb^2 blocks per
- * image of nb = ceil(n_b / 256) blocks under the full schedule and
- * nb (nb + 1) / 2 under the symmetric one. Rows whose byte length is not a
- * multiple of 64 always report MPM_SCHEDULE_FULL. Returns MPM_OK,
+ * The schedule (MPM_SCHEDULE_FULL, MPM_SCHEDULE_SYMMETRIC or
+ * MPM_SCHEDULE_FULL_64, never AUTO) that mpm_affinity would run for B images
+ * of at most N tokens of D channels of dtype dt on the current device under
+ * the current mode, written to *schedule (a host pointer). For reporting the
+ * matrix-core work a call issues: about 2 * w^2 * D flops per w x w block,
+ * nb^2 blocks per image of nb = ceil(n_b / w) blocks under the full schedules
+ * (w = 256, or 64 for MPM_SCHEDULE_FULL_64) and nb (nb + 1) / 2 under the
+ * symmetric one (w = 256). Rows whose byte length is not a multiple of 64
+ * always report MPM_SCHEDULE_FULL. Returns MPM_OK,
  * MPM_ERR_INVALID_ARG for bad sizes or a NULL pointer, or MPM_ERR_HIP when
  * the device cannot be queried.
  */

@@ -23,6 +23,7 @@ MPM_BF16 = 1
 MPM_SCHEDULE_AUTO = 0
 MPM_SCHEDULE_FULL = 1
 MPM_SCHEDULE_SYMMETRIC = 2
+MPM_SCHEDULE_FULL_64 = 3
 
 _vp = ctypes.c_void_p
 _i32 = ctypes.c_int32

@@ -103,12 +103,13 @@ def workspace_bytes(B: int, N: int) -> int:
     return int(_lib.load().mpm_workspace_bytes(B, N))
 
 
-SCHEDULES = {"auto": _lib.MPM_SCHEDULE_AUTO, "full": _lib.MPM_SCHEDULE_FULL, "symmetric": _lib.MPM_SCHEDULE_SYMMETRIC}
+SCHEDULES = {"auto": _lib.MPM_SCHEDULE_AUTO, "full": _lib.MPM_SCHEDULE_FULL, "symmetric": _lib.MPM_SCHEDULE_SYMMETRIC,
+             "full_64": _lib.MPM_SCHEDULE_FULL_64}
 
 
 def set_affinity_schedule(mode: str) -> str:
-    """Select the affinity kernel's work schedule ("auto", "full" or "symmetric",
-    process-wide); returns the previous one. Results do not depend on it."""
+    """Select the affinity kernel's work schedule ("auto", "full", "symmetric" or
+    "full_64", process-wide); returns the previous one. Results do not depend on it."""
     if mode not in SCHEDULES:
         raise ValueError(f"unknown schedule {mode!r}; expected one of {sorted(SCHEDULES)}")
     prev = _lib.load().mpm_set_affinity_schedule(SCHEDULES[mode])
@@ -118,8 +119,8 @@ def set_affinity_schedule(mode: str) -> str:
 
 
 def affinity_schedule_used(B: int, N: int, D: int, dtype: torch.dtype) -> str:
-    """The schedule ("full" or "symmetric") the affinity kernel runs for this shape
-    on the current device under the current mode."""
+    """The schedule ("full", "symmetric" or "full_64") the affinity kernel runs for
+    this shape on the current device under the current mode."""
     out = ctypes.c_int32()
     _lib.check("mpm_affinity_schedule_used",
                _lib.load().mpm_affinity_schedule_used(B, N, D, _DTYPES[dtype], ctypes.byref(out)))

@@ -579,15 +579,20 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     // chunk ends).
     constexpr int PGROUPS = KG * MT * NT;  // MFMAs per chunk
     constexpr int PSPAN = STAGES >= 3 ? PGROUPS : PGROUPS / 2;
-    static_assert(PSPAN >= LOADS && PSPAN % LOADS == 0, "load parts per MFMA");
-    constexpr int PSTEP = PSPAN / LOADS;
+    static_assert(PSPAN >= 1 && (PSPAN < LOADS || PSPAN % LOADS == 0), "load parts per MFMA");
+    constexpr int PSTEP = PSPAN >= LOADS ? PSPAN / LOADS : 1;              // MFMAs between load slots
+    constexpr int PPER = PSPAN >= LOADS ? 1 : (LOADS + PSPAN - 1) / PSPAN;  // loads per slot (small tiles)
     auto mma_issue = [&](const u32x4 (&fa)[MT], const u32x4 (&fq)[NT], int g) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
                 const int p = (g * MT + mt) * NT + nt;
-                if (p % PSTEP == 0 && p / PSTEP < LOADS) issue_part(p / PSTEP);
+                if (p % PSTEP == 0) {
+#pragma unroll
+                    for (int q = 0; q < PPER; ++q)
+                        if ((p / PSTEP) * PPER + q < LOADS) issue_part((p / PSTEP) * PPER + q);
+                }
                 Mfma<S>::mma(acc[mt][nt], fa[mt], fq[nt]);
             }
             // Candidate norms: m-tile mt is summed by the wave with wq == mt % WQ only.
@@ -911,6 +916,12 @@ constexpr int kPWC = 2, kPWQ = 4, kPMT = 4, kPNT = 2, kPCB = 64, kPWGS = 1;
 constexpr int kPCB2 = 128;
 constexpr int kSWC = 4, kSWQ = 2, kSMT = 2, kSNT = 4;
 constexpr int kPCT = kPWC * kPMT * 32;
+// Small batches (few 256 x 256 blocks for the device's CUs) use 64 x 64 blocks on 4 waves
+// of one 32 x 32 tile each, so a single image of 1024 tokens still spreads over 256 CUs.
+constexpr int kTWC = 2, kTWQ = 2, kTMT = 1, kTNT = 1;
+constexpr int kTCT = kTWC * kTMT * 32;
+constexpr long kSmallItems = 32;  // batches with at most this many 256 x 256 blocks take them
+static_assert(kTWQ * kTNT * 32 == kTCT && kPCT % kTCT == 0, "square small blocks that nest in the large ones");
 static_assert(kSWC * kSMT * 32 == kPCT && kSWQ * kSNT * 32 == kPCT && kPWQ * kPNT * 32 == kPCT,
               "both schedules use 256 x 256 tiles, so their partials share one layout");
 
@@ -957,13 +968,28 @@ hipError_t launch_staged(const void* x, const int32_t* x_off, int B, int N, int 
 
 }  // namespace
 
-int partial_tiles(int N) { return (N + kPCT - 1) / kPCT; }
+// Partial slots reserved per token: enough for the smallest block width any schedule uses.
+int partial_tiles(int N) { return (N + kTCT - 1) / kTCT; }
 
-int partial_tile_width(int D, int dt, int N) { return use_persistent(D, dt) ? kPCT : N; }
+// Whether a persistent launch of this shape uses the 64 x 64 blocks (no device query).
+bool small_blocks(int B, int N)
+{
+    const int mode = g_schedule.load();
+    if (mode != kScheduleAuto) return mode == kScheduleFull64;
+    const long nqb = (N + kPCT - 1) / kPCT;
+    return (long)B * nqb * nqb <= kSmallItems;
+}
+
+int partial_tile_width(int B, int D, int dt, int N)
+{
+    if (!use_persistent(D, dt)) return N;
+    return small_blocks(B, N) ? kTCT : kPCT;
+}
 
 int set_affinity_schedule(int mode)
 {
-    if (mode != kScheduleAuto && mode != kScheduleFull && mode != kScheduleSymmetric) return -1;
+    if (mode != kScheduleAuto && mode != kScheduleFull && mode != kScheduleSymmetric && mode != kScheduleFull64)
+        return -1;
     return g_schedule.exchange(mode);
 }
 
@@ -985,6 +1011,10 @@ hipError_t affinity_schedule(int B, int N, int D, int dt, int* schedule)
 {
     *schedule = kScheduleFull;
     if (!use_persistent(D, dt)) return hipSuccess;  // the staged kernel covers every pair
+    if (small_blocks(B, N)) {
+        *schedule = kScheduleFull64;
+        return hipSuccess;
+    }
     const int cus = device_cus();
     if (cus <= 0) return hipErrorInvalidDevice;
     const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
@@ -1003,6 +1033,15 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
         // workgroups by XCD.
         const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
         const int groups = cus * kPWGS;
+        if (small_blocks(B, N)) {
+            if (dt == kBf16)
+                launch_persistent<Bf16, kTWC, kTWQ, kTMT, kTNT, false>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                                                                        stream, start, stop);
+            else
+                launch_persistent<F32, kTWC, kTWQ, kTMT, kTNT, false>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                                                                       stream, start, stop);
+            return hipGetLastError();
+        }
         const bool sym = symmetric_schedule(B, N, xcds, groups / xcds);
         if (dt == kBf16) {
             if (sym)

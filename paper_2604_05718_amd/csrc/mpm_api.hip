@@ -91,15 +91,20 @@ hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 // nb from the affinity partials, then mutual pairs and compact ids. With few
 // candidate tiles the compaction kernel (one workgroup per image) reduces the
 // partials itself; with more, that serial reduction dominates, so a fully
-// parallel reduction writes nb first and the compaction reads it.
+// parallel reduction writes nb first and the compaction reads it. A batch of a
+// few images (as small as the 64 x 64 block schedule is for) leaves most of
+// the device idle either way, and one launch fewer wins up to 16 tiles.
 constexpr int kFusedReduceMaxTiles = 4;
+constexpr int kFusedReduceMaxTilesFewImages = 16;
+constexpr int kFewImages = 8;
 
 hipError_t compact_from_partials(const Workspace& w, const int32_t* x_off, int32_t B, int32_t N, int32_t D,
                                  int32_t dt, int32_t* map, hipStream_t st)
 {
     const int T = mpm::partial_tiles(N);
-    const int ct = mpm::partial_tile_width(D, dt, N);
-    if ((N + ct - 1) / ct <= kFusedReduceMaxTiles)
+    const int ct = mpm::partial_tile_width(B, D, dt, N);
+    const int fused_max = B <= kFewImages ? kFusedReduceMaxTilesFewImages : kFusedReduceMaxTiles;
+    if ((N + ct - 1) / ct <= fused_max)
         return mpm::launch_pair_compact_partials(w.pv, w.pi, T, ct, w.nb, x_off, B, N, map, w.src, w.count, st);
     hipError_t e = mpm::launch_reduce_partials(w.pv, w.pi, nullptr, x_off, B, N, D, dt, w.nb, nullptr, st);
     if (e == hipSuccess) e = mpm::launch_pair_compact(w.nb, x_off, B, N, map, w.src, w.count, st);

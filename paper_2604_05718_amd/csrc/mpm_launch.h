@@ -13,16 +13,17 @@ enum Dtype : int { kF32 = 0, kBf16 = 1 };
 // start/stop (may be null) are bound to the kernel's own dispatch (hipExtLaunchKernel).
 hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, int D, int dt, float* pv,
                            int32_t* pi, hipStream_t stream, hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
+// Partial slots per token in the workspace (the tile stride of pv/pi): ceil(N / 64).
 int partial_tiles(int N);
-// Candidate rows covered by one partial of the kernel launch_affinity picks.
-int partial_tile_width(int D, int dt, int N);
+// Candidate rows covered by one partial of the kernel launch_affinity picks for B images.
+int partial_tile_width(int B, int D, int dt, int N);
 // Work schedule of the persistent affinity kernel: every (query block, candidate
 // tile) pair, only the pairs on and above the diagonal (the symmetric schedule),
 // or a choice by batch shape. Process-wide; returns the previous mode, or -1 (and
 // changes nothing) for an unknown mode.
-enum AffinitySchedule : int { kScheduleAuto = 0, kScheduleFull = 1, kScheduleSymmetric = 2 };
+enum AffinitySchedule : int { kScheduleAuto = 0, kScheduleFull = 1, kScheduleSymmetric = 2, kScheduleFull64 = 3 };
 int set_affinity_schedule(int mode);
-// The schedule (kScheduleFull or kScheduleSymmetric) launch_affinity would run
+// The schedule (kScheduleFull, kScheduleSymmetric or kScheduleFull64) launch_affinity would run
 // for this shape on the current device under the current mode.
 hipError_t affinity_schedule(int B, int N, int D, int dt, int* schedule);
 hipError_t launch_reduce_partials(const float* pv, const int32_t* pi, const void* x, const int32_t* x_off, int B,

@@ -234,7 +234,7 @@ hipError_t launch_reduce_partials(const float* pv, const int32_t* pi, const void
                                   int N, int D, int dt, int32_t* nb, float* best, hipStream_t stream)
 {
     const int T = partial_tiles(N);
-    const int ct = partial_tile_width(D, dt, N);
+    const int ct = partial_tile_width(B, D, dt, N);
     const long total = (long)B * N;
     const dim3 grid((unsigned)((total + 255) / 256));
     const uint8_t* xp = static_cast<const uint8_t*>(x);

@@ -35,7 +35,7 @@ def test_version_and_status_strings(lib):
 def test_workspace_bytes_and_offsets(lib):
     r = lambda v: (v + 255) // 256 * 256
     for B, N in [(64, 1024), (16, 4096), (3, 5), (1, 257)]:
-        T = (N + 255) // 256
+        T = (N + 63) // 64  # partial slots per token, include/mpm.h
         want = r(4 * B * N) + r(8 * B * N) + r(4 * B) + r(4 * B * T * N) + r(4 * B * T * N)
         assert lib.mpm_workspace_bytes(B, N) == want
         off = _lib.workspace_offsets(B, N)
@@ -104,15 +104,17 @@ def test_other_entry_points_reject(lib):
 
 
 def test_affinity_schedule_knob(lib):
-    """Host-only: the schedule setter returns the previous mode, accepts the three
+    """Host-only: the schedule setter returns the previous mode, accepts the four
     mpm_schedule values and rejects anything else without changing the mode."""
     prev = lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_FULL)
     try:
-        assert prev in (_lib.MPM_SCHEDULE_AUTO, _lib.MPM_SCHEDULE_FULL, _lib.MPM_SCHEDULE_SYMMETRIC)
+        assert prev in (_lib.MPM_SCHEDULE_AUTO, _lib.MPM_SCHEDULE_FULL, _lib.MPM_SCHEDULE_SYMMETRIC,
+                        _lib.MPM_SCHEDULE_FULL_64)
         assert lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_SYMMETRIC) == _lib.MPM_SCHEDULE_FULL
-        for bad in (-1, 3, 1 << 20):
+        assert lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_FULL_64) == _lib.MPM_SCHEDULE_SYMMETRIC
+        for bad in (-1, 4, 1 << 20):
             assert lib.mpm_set_affinity_schedule(bad) == -1
-        assert lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_AUTO) == _lib.MPM_SCHEDULE_SYMMETRIC
+        assert lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_AUTO) == _lib.MPM_SCHEDULE_FULL_64
     finally:
         lib.mpm_set_affinity_schedule(prev)
     out = ctypes.c_int32(-7)

@@ -423,7 +423,7 @@ def _affinity_partials(x2, x_off, B, N, D, dtype):
                                                         _stream()))
     torch.cuda.synchronize()
     o = _lib.workspace_offsets(B, N)
-    T = (N + 255) // 256
+    T = (N + 63) // 64  # partial slots per token (the workspace layout of include/mpm.h)
     pv = ws[o["pv"]:o["pv"] + 4 * B * T * N].view(torch.float32).view(B, T, N).cpu().numpy()
     pi = ws[o["pi"]:o["pi"] + 4 * B * T * N].view(torch.int32).view(B, T, N).cpu().numpy()
     return pv, pi
@@ -516,3 +516,72 @@ def test_merge_many_tiles_both_schedules(dtype, schedule):
     y_off = res.y_off.cpu().numpy()
     for b, n in enumerate(ns):
         check_stage(to64(rows[b]), dtype, nb[b, :n], m[b], to64(y[y_off[b]:y_off[b + 1]]))
+
+
+def _small_block_case(name, dtype):
+    """(rows per image, N, D) of the 64 x 64 block cases."""
+    rng = np.random.default_rng(zlib.crc32(("small-" + name).encode()))
+    if name == "one_image_1024":  # the ViT-Ti shape, scaled down in D
+        return [store(clustered(rng, 1024, 64, k=12), dtype)], 1024, 64
+    if name == "dense_300":  # ragged last block inside each image
+        return [store(clustered(rng, 300, 96, k=10), dtype) for _ in range(2)], 300, 96
+    if name == "duplicated_rows":  # exact ties across 64-row blocks
+        h = clustered(rng, 100, 64, k=8)
+        return [store(np.repeat(h, 2, axis=0), dtype)], 200, 64
+    if name == "packed_ragged":
+        ns = [1, 64, 65, 130, 500, 2]
+        return [store(clustered(rng, n, 64, k=6), dtype) for n in ns], 500, 64
+    raise KeyError(name)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("name", ["one_image_1024", "dense_300", "duplicated_rows", "packed_ragged"])
+def test_small_blocks_equal_full_schedule(dtype, name):
+    """The 64 x 64 block schedule (small batches) must give the same nearest
+    neighbours and cosines, bit for bit, as the full schedule on 256 x 256
+    blocks (every score comes from the same MFMA sums; the lexicographic
+    reduction over tiles does not depend on the tile width), and they must pass
+    the oracle parity check."""
+    rows, N, D = _small_block_case(name, dtype)
+    ns = [r.shape[0] for r in rows]
+    B = len(rows)
+    print(f"small blocks {name} {dtype} ns={ns} D={D}", flush=True)
+    packed = name == "packed_ragged"
+    if packed:
+        x = torch.cat(rows).to(DEV)
+        x_off = torch.from_numpy(np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)).to(DEV)
+    else:
+        x = torch.stack(rows).to(DEV)
+        x_off = None
+    out = {}
+    for mode in ("full", "full_64"):
+        prev = mpm.set_affinity_schedule(mode)
+        try:
+            assert mpm.affinity_schedule_used(B, N, D, x.dtype) == mode
+            nb, best = mpm.argmax(x, x_off=x_off, N=N if packed else None, with_best=True)
+            torch.cuda.synchronize()
+            out[mode] = (nb.cpu().numpy(), best.cpu().numpy())
+        finally:
+            mpm.set_affinity_schedule(prev)
+    (fn, fb), (sn, sb) = out["full"], out["full_64"]
+    for b, n in enumerate(ns):
+        assert np.array_equal(fn[b, :n], sn[b, :n]), b
+        assert np.array_equal(fb[b, :n].view(np.uint32), sb[b, :n].view(np.uint32)), b
+        if n == 1:
+            assert sn[b, 0] == -1
+            continue
+        check_nearest(to64(rows[b]), sn[b, :n])
+
+
+def test_small_blocks_chosen_for_small_batches():
+    """Auto mode takes the 64 x 64 blocks when a batch has at most 32 blocks of
+    256 x 256 (rows a multiple of 64 bytes), and the large blocks otherwise."""
+    prev = mpm.set_affinity_schedule("auto")
+    try:
+        assert mpm.affinity_schedule_used(1, 1024, 192, torch.float32) == "full_64"
+        assert mpm.affinity_schedule_used(2, 1024, 768, torch.bfloat16) == "full_64"
+        assert mpm.affinity_schedule_used(3, 1024, 768, torch.bfloat16) != "full_64"
+        assert mpm.affinity_schedule_used(1, 4096, 1024, torch.bfloat16) != "full_64"
+        assert mpm.affinity_schedule_used(1, 1024, 24, torch.bfloat16) == "full"  # 48-byte rows: no schedule choice
+    finally:
+        mpm.set_affinity_schedule(prev)
