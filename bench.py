@@ -32,8 +32,8 @@ AFF_SAMPLE = 8   # every 8th timed step carries the affinity kernels' timing eve
 # HBM traffic of the affinity-argmax kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "bc572f5770bd771e3943ca8d123049971a244d4f5961000773c44750d142fcfd",
-           "bytes_per_launch": 107434003}
+TRAFFIC = {"source_sha256": "ff1d2d59e093784107d41d1a816c16a495b046c5a0b2d0655f3bdcbb5227e844",
+           "bytes_per_launch": 107527273}
 
 
 def log(*a):
