@@ -585,3 +585,48 @@ def test_small_blocks_chosen_for_small_batches():
         assert mpm.affinity_schedule_used(1, 1024, 24, torch.bfloat16) == "full"  # 48-byte rows: no schedule choice
     finally:
         mpm.set_affinity_schedule(prev)
+
+
+# ---- the largest sizes the C ABI accepts -----------------------------------------
+
+@pytest.mark.parametrize("case", ["max_tokens", "max_channels"])
+def test_maximum_sizes(case):
+    """Two insertions, composition and gather at N = MPM_MAX_N (compaction LDS of
+    128 KB, 64 partial tiles per token) and at D = MPM_MAX_D (32 KB rows), checked
+    stage by stage and end to end against the oracle."""
+    rng = np.random.default_rng(zlib.crc32(case.encode()))
+    if case == "max_tokens":
+        B, N, D, k = 1, 16384, 64, 200
+    else:
+        B, N, D, k = 2, 300, 16384, 12
+    print(f"maximum sizes {case}: B={B} N={N} D={D} bf16", flush=True)
+    x = torch.stack([store(clustered(rng, N, D, k=k, sigma=0.3), "bf16") for _ in range(B)])
+    res = mpm.run_schedule(x.to(DEV), insertions=2)
+    torch.cuda.synchronize()
+    for b in range(B):
+        reps = check_schedule_image(x[b], "bf16", res, b)
+        print(f"  image {b}: " + ", ".join(f"n={r.n} n'={r.count} flips={r.flipped_rows}" for r in reps), flush=True)
+
+
+def test_many_images():
+    """20000 images of 4 tokens (64-byte rows): every image's merge against the
+    oracle, so the per-XCD grouping of the affinity kernel and the one-workgroup-
+    per-image kernels run at a batch far beyond the CU count."""
+    rng = np.random.default_rng(77)
+    B, N, D = 20000, 4, 32
+    x64 = rng.standard_normal((B, N, D))
+    x = store(x64.reshape(B * N, D), "bf16").view(B, N, D)
+    print(f"many images: B={B} N={N} D={D} bf16", flush=True)
+    m = mpm.merge(x.to(DEV))
+    torch.cuda.synchronize()
+    nb = m.nb.cpu().numpy()
+    maps = m.map.cpu().numpy()
+    y_off = m.y_off.cpu().numpy()
+    y = m.y.cpu().to(torch.float64).numpy()
+    xs = to64(x)
+    for b in range(B):
+        check_nearest(xs[b], nb[b], threads=1)  # raises on anything but an accepted near-tie
+        ref = oracle.merge(xs[b], "bf16", threads=1, nb=nb[b])
+        assert np.array_equal(maps[b], ref.map), b
+        assert y_off[b + 1] - y_off[b] == ref.count, b
+        assert rel_err(y[y_off[b]:y_off[b + 1]], ref.y) <= 2e-2, b
