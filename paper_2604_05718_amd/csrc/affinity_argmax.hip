@@ -445,7 +445,8 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     const int group = blockIdx.x % xcds;
     const int slot = blockIdx.x / xcds;
     const int nqb = (N + QT - 1) / QT;
-    const int per_img = SYM ? nqb * (nqb + 1) / 2 : nqb * T;
+    const int nct = (N + CT - 1) / CT;  // candidate tiles per image (T, the slot stride, may be larger)
+    const int per_img = SYM ? nqb * (nqb + 1) / 2 : nqb * nct;
     const int nimg = (B - group + xcds - 1) / xcds;
     const int nitems = nimg * per_img;
     const long rowbytes = (long)D * S::kBytes;
@@ -469,8 +470,8 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                 }
                 t = qb + w;
             } else {
-                qb = w / T;
-                t = w - qb * T;
+                qb = w / nct;
+                t = w - qb * nct;
             }
             const int b = group + xcds * ib;
             const int row0 = x_off ? x_off[b] : b * N;

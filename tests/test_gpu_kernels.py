@@ -587,6 +587,47 @@ def test_small_blocks_chosen_for_small_batches():
         mpm.set_affinity_schedule(prev)
 
 
+def _affinity_us(x, B, N, D, reps=9):
+    """Median duration (microseconds) of mpm_affinity_timed over reps launches."""
+    from paper_2604_05718_amd import _lib
+    from paper_2604_05718_amd.api import _p, _stream
+    lib = _lib.load()
+    ws = torch.empty((mpm.workspace_bytes(B, N),), dtype=torch.uint8, device=DEV)
+    dt = _lib.MPM_BF16 if x.dtype == torch.bfloat16 else _lib.MPM_F32
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps + 1)]
+    for a, b in ev:  # torch creates the underlying events on first record
+        a.record()
+        b.record()
+    for a, b in ev:
+        _lib.check("mpm_affinity_timed", lib.mpm_affinity_timed(_p(x), None, B, N, D, dt, _p(ws), ws.numel(),
+                                                                a.cuda_event, b.cuda_event, _stream()))
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) * 1e3 for a, b in ev[1:]]))
+
+
+def test_full_schedule_spreads_items():
+    """At B = 32, N = 1024, D = 384 (bf16) both 256 x 256 schedules hand every
+    workgroup slot about two items (full: 16 per image, symmetric: 10 per image,
+    on 32 slots per group of 4 images), so their launches take about as long.
+    Items enumerated over the workspace's partial slots (ceil(N / 64) per token)
+    instead of the 256-wide tiles left three quarters of the full schedule's
+    items empty and piled its real ones on a quarter of the slots (3x slower);
+    this guards the balance that parity tests cannot see."""
+    B, N, D = 32, 1024, 384
+    g = torch.Generator().manual_seed(11)
+    x = torch.randn((B, N, D), generator=g).to(torch.bfloat16).to(DEV)
+    us = {}
+    for mode in ("full", "symmetric"):
+        prev = mpm.set_affinity_schedule(mode)
+        try:
+            assert mpm.affinity_schedule_used(B, N, D, x.dtype) == mode
+            us[mode] = _affinity_us(x, B, N, D)
+        finally:
+            mpm.set_affinity_schedule(prev)
+    print(f"affinity B={B} N={N} D={D}: full {us['full']:.1f} us, symmetric {us['symmetric']:.1f} us", flush=True)
+    assert us["full"] < 1.6 * us["symmetric"], us
+
+
 # ---- the largest sizes the C ABI accepts -----------------------------------------
 
 @pytest.mark.parametrize("case", ["max_tokens", "max_channels"])
