@@ -32,8 +32,8 @@ AFF_SAMPLE = 8   # every 8th timed step carries the affinity kernels' timing eve
 # HBM traffic of the affinity-argmax kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "ff1d2d59e093784107d41d1a816c16a495b046c5a0b2d0655f3bdcbb5227e844",
-           "bytes_per_launch": 107527273}
+TRAFFIC = {"source_sha256": "d0ffe77cc9076c7d8c481d0413aa6340366497a074c0b840457a0bd426937e51",
+           "bytes_per_launch": 107469470}
 
 
 def log(*a):
