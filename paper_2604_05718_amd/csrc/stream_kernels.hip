@@ -15,7 +15,7 @@ namespace mpm {
 namespace {
 
 constexpr int kRowThreads = 256;
-constexpr int kRowBytesPerBlock = 32768;     // output bytes one workgroup handles
+constexpr int kRowBytesPerBlock = 8192;      // output bytes one workgroup handles
 constexpr int kGatherBytesPerBlock = 16384;  // ... in the gather, which first resolves its rows' sources
 // Vectors each thread loads before storing them (loads in flight per thread).
 constexpr int kGatherBatch = 4;
