@@ -29,11 +29,12 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak"
 AFF_SAMPLE = 8   # every 8th timed step carries the affinity kernels' timing events
 
-# HBM traffic of the affinity-argmax kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
+# HBM traffic of one affinity step (the whole-block launch and, where the schedule
+# defers diagonal blocks, the half-block launch) from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "d0ffe77cc9076c7d8c481d0413aa6340366497a074c0b840457a0bd426937e51",
-           "bytes_per_launch": 107469470}
+TRAFFIC = {"source_sha256": "111a37e1c9290d6de885502254835c5648ac9c6fd77f1bfb04ac80a4229b50a2",
+           "bytes_per_launch": 149372361}
 
 
 def log(*a):
@@ -140,6 +141,8 @@ def main() -> int:
                     help="budget of the CPU oracle baseline (0 skips it)")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="steps timed after evicting the caches (0 skips them)")
+    ap.add_argument("--schedule", default="auto", choices=["auto", "full", "symmetric", "full_64"],
+                    help="affinity work schedule (auto: the library's choice for the batch shape)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run 5 device-to-device copies of this many MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -168,6 +171,7 @@ def main() -> int:
     from paper_2604_05718_amd import api, synth
 
     cfg = synth.config(args.workload)
+    mpm.set_affinity_schedule(args.schedule)
     dev = torch.device("cuda:0")
     dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     log(f"bench: {cfg.name} B={cfg.B} N={cfg.N} D={cfg.D} {cfg.dtype}, generating inputs")

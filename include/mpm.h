@@ -127,13 +127,16 @@ int mpm_affinity(const void* x, const int32_t* x_off, int32_t B, int32_t N, int3
                  size_t ws_bytes, void* stream);
 
 /*
- * mpm_affinity with its kernel's execution interval recorded into two events,
- * for callers that time the dominant kernel of a step (telemetry, profiling)
+ * mpm_affinity with its execution interval recorded into two events, for
+ * callers that time the dominant kernel of a step (telemetry, profiling)
  * without adding stream commands between kernels. start_event / stop_event
  * are hipEvent_t the caller created (timing enabled) and owns; either may be
- * NULL. They are bound to the kernel's own dispatch (hipExtLaunchKernel), so
- * hipEventElapsedTime(start, stop) is that kernel's duration. Same results,
- * arguments and errors as mpm_affinity otherwise.
+ * NULL. They are bound to the kernels' own dispatches (hipExtLaunchKernel):
+ * start to the first launch, stop to the last. The step is one launch, or two
+ * when the symmetric schedule runs its deferred diagonal blocks as half blocks
+ * in a second launch (see mpm_set_affinity_schedule), so
+ * hipEventElapsedTime(start, stop) is the step's duration on the device. Same
+ * results, arguments and errors as mpm_affinity otherwise.
  */
 int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* ws,
                        size_t ws_bytes, void* start_event, void* stop_event, void* stream);
@@ -145,7 +148,11 @@ int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N
  * (Eq. 1), so the symmetric schedule computes only the 256 x 256 blocks on and
  * above the block diagonal and takes each off-diagonal block's argmax in both
  * directions, about half the matrix-core work for large images at the price of
- * a cross-lane reduction per block. MPM_SCHEDULE_FULL_64 computes every pair of
+ * a cross-lane reduction per block. For rows that are a whole number of
+ * 128-byte chunks, when an XCD group's blocks would leave a last round on at
+ * most half of its workgroups, that many diagonal blocks are deferred to a
+ * second launch that runs each as two halves of its queries, one per
+ * workgroup. MPM_SCHEDULE_FULL_64 computes every pair of
  * 64 x 64 blocks, so that a small batch (a single image of 1024 tokens has 16
  * blocks of 256 x 256 but 256 of 64 x 64) still occupies every compute unit.
  * MPM_SCHEDULE_AUTO (the default) takes the 64 x 64 blocks when the batch has

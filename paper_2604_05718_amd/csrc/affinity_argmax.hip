@@ -405,7 +405,24 @@ __device__ __forceinline__ void exchange_half(float* v, int32_t* ix, int upper)
 // directly, so the partials are bit-identical to the full schedule's. Items are
 // taken image by image, the blocks of an image row by row, so all the items of
 // an image still run together on one XCD and share its L2.
-template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES, bool SYM>
+// Diagonal blocks taken out of a group's symmetric-schedule order (see HALVES below): with
+// `whole` items on `slots` workgroups the last round holds m = whole mod slots items; when
+// 0 < 2m <= slots and the group has at least m diagonal blocks, m of them are deferred.
+__host__ __device__ inline int deferred_diagonals(int nimg, int nb, int slots)
+{
+    const int whole = nimg * (nb * (nb + 1) / 2);
+    const int m = whole % slots;
+    return (m > 0 && 2 * m <= slots && m <= nimg * nb) ? m : 0;
+}
+
+// HALVES: the second launch of a symmetric schedule on the two-stage ring. The first
+// launch (SYM) leaves out the last deferred_diagonals() diagonal blocks of its XCD group
+// (all of the last images', then the last ones of the image before), so that its slots
+// take whole rounds; this launch runs each deferred block as two items of the block's
+// 256 candidates and one half of its queries (QT = CT/2). A diagonal block needs no
+// reverse direction, so the two halves write disjoint query partials, and each score
+// comes from the same MFMA sequence as in a whole block.
+template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES, bool SYM, bool HALVES = false>
 __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  // 2 waves per SIMD
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int T, int xcds,
     int slots, float* __restrict__ pv, int32_t* __restrict__ pi)
@@ -417,9 +434,12 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     static_assert(CB == 64 || CB == 128, "swizzled layouts exist for 64- and 128-byte row chunks");
     constexpr int NS = CB / 16;                       // 16-byte slots per row
     constexpr int RPI = 64 / NS;                      // rows per load instruction (1 KB)
-    constexpr int GROUPS = (CT + QT) / RPI;           // load instructions per stage
+    // Rows a stage holds: the candidate tile, then the query block (none for a half item,
+    // whose queries are rows of its own candidate tile).
+    constexpr int QROWS = HALVES ? 0 : QT;
+    constexpr int GROUPS = (CT + QROWS) / RPI;        // load instructions per stage
     constexpr int LOADS = GROUPS / WAVES;             // ... per wave
-    constexpr int STAGE_BYTES = (CT + QT) * CB;
+    constexpr int STAGE_BYTES = (CT + QROWS) * CB;
     constexpr int KG = CB / 32;                       // 32-byte k-groups (one MFMA k-step each) per chunk
     static_assert(GROUPS % WAVES == 0 && CT % RPI == 0 && CT % 32 == 0 && QT % 32 == 0, "stage/wave mismatch");
     static_assert(STAGES >= 2 && (STAGES - 2) * LOADS < 64, "pipeline depth / vmcnt range");
@@ -448,7 +468,13 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     const int nct = (N + CT - 1) / CT;  // candidate tiles per image (T, the slot stride, may be larger)
     const int per_img = SYM ? nqb * (nqb + 1) / 2 : nqb * nct;
     const int nimg = (B - group + xcds - 1) / xcds;
-    const int nitems = nimg * per_img;
+    static_assert(!HALVES || (!SYM && 2 * QT == CT), "half items: forward only, half a block of queries");
+    constexpr bool SPLIT = SYM && STAGES == 2;  // the layouts the second launch exists for
+    const int ndef = (SPLIT || HALVES) ? deferred_diagonals(nimg, nct, slots) : 0;
+    const int dfull = ndef / nct, dpart = ndef % nct;
+    const int dimg = nimg - dfull - 1;                        // the image with dpart deferred
+    const int upto_dimg = (dimg + 1) * per_img - dpart;       // first-launch items of images 0..dimg
+    const int nitems = HALVES ? 2 * ndef : nimg * per_img - ndef;
     const long rowbytes = (long)D * S::kBytes;
     const int nchunks = (int)(rowbytes / CB);
 
@@ -459,25 +485,51 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     auto find = [&](int k) {
         Item it;
         for (; k < nitems; k += slots) {
-            const int ib = k / per_img;
-            int w = k - ib * per_img;
-            int qb, t;
-            if (SYM) {  // blocks qb <= t of the upper triangle, row by row
-                qb = 0;
-                while (w >= nqb - qb) {
-                    w -= nqb - qb;
+            int ib, qbase, t;
+            if (HALVES) {  // deferred diagonal e, query half k % 2
+                const int e = k >> 1;
+                int qb;
+                if (e < dpart) {
+                    ib = dimg;
+                    qb = nct - dpart + e;
+                } else {
+                    ib = dimg + 1 + (e - dpart) / nct;
+                    qb = (e - dpart) - (ib - dimg - 1) * nct;
+                }
+                t = qb;
+                qbase = qb * CT + (k & 1) * QT;
+            } else if (SYM) {  // blocks qb <= t of the upper triangle, row by row, minus deferred diagonals
+                int w;
+                if (k < upto_dimg) {
+                    ib = k / per_img;
+                    w = k - ib * per_img;
+                } else {
+                    const int rest = max(1, per_img - nqb);
+                    ib = dimg + 1 + (k - upto_dimg) / rest;
+                    w = (k - upto_dimg) - (ib - dimg - 1) * rest;
+                }
+                const int d = ib > dimg ? nqb : (ib == dimg ? dpart : 0);  // image ib's deferred diagonals
+                int qb = 0;
+                for (;;) {
+                    const int len = nqb - qb - (qb >= nqb - d ? 1 : 0);
+                    if (w < len) break;
+                    w -= len;
                     ++qb;
                 }
-                t = qb + w;
+                t = qb + w + (qb >= nqb - d ? 1 : 0);
+                qbase = qb * QT;
             } else {
-                qb = w / nct;
+                ib = k / per_img;
+                const int w = k - ib * per_img;
+                const int qb = w / nct;
                 t = w - qb * nct;
+                qbase = qb * QT;
             }
             const int b = group + xcds * ib;
             const int row0 = x_off ? x_off[b] : b * N;
             const int n = x_off ? x_off[b + 1] - row0 : N;
-            if (qb * QT < n && t * CT < n) {
-                it.k = k; it.b = b; it.qbase = qb * QT; it.cbase = t * CT; it.n = n; it.row0 = row0;
+            if (qbase < n && t * CT < n) {
+                it.k = k; it.b = b; it.qbase = qbase; it.cbase = t * CT; it.n = n; it.row0 = row0;
                 return it;
             }
         }
@@ -553,7 +605,12 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     // Row lrow of every 32-row fragment has the same swizzle (32 is a multiple of 16).
     const int sw = swz(lrow & 15);
     const int lc_off = (wc * MT * 32 + lrow) * CB;
-    const int lq_off = (CT + wq * NT * 32 + lrow) * CB;
+    // A half item's queries are rows qbase - cbase.. of its candidate tile. Its first value
+    // comes from the issue cursor's first item, which is the compute cursor's first item
+    // (the prologue of a deeper ring reads fragments before the compute cursor exists); a
+    // slot runs at most one half item (2 * ndef <= slots), so the read-ahead of a next
+    // chunk never crosses into another half item.
+    int lq_off = (HALVES ? ii.qbase - ii.cbase : CT) * CB + (wq * NT * 32 + lrow) * CB;
     u32x4 fa0[MT], fq0[NT], fa1[MT], fq1[NT];
     auto read_frags = [&](u32x4 (&fa)[MT], u32x4 (&fq)[NT], int chunk, int g) {
         const uint8_t* sb = lds + (chunk % STAGES) * STAGE_BYTES;
@@ -580,7 +637,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     // chunk ends).
     constexpr int PGROUPS = KG * MT * NT;  // MFMAs per chunk
     constexpr int PSPAN = STAGES >= 3 ? PGROUPS : PGROUPS / 2;
-    static_assert(PSPAN >= 1 && (PSPAN < LOADS || PSPAN % LOADS == 0), "load parts per MFMA");
+    static_assert(PSPAN >= 1, "load parts per MFMA");
     constexpr int PSTEP = PSPAN >= LOADS ? PSPAN / LOADS : 1;              // MFMAs between load slots
     constexpr int PPER = PSPAN >= LOADS ? 1 : (LOADS + PSPAN - 1) / PSPAN;  // loads per slot (small tiles)
     auto mma_issue = [&](const u32x4 (&fa)[MT], const u32x4 (&fq)[NT], int g) {
@@ -901,6 +958,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         }
         cchunk = 0;
         ci = find(ci.k + slots);
+        if constexpr (HALVES) lq_off = (ci.qbase - ci.cbase + wq * NT * 32 + lrow) * CB;
     }
 }
 
@@ -938,16 +996,34 @@ int device_cus()
     return cus;
 }
 
+// Whether a symmetric launch on the two-stage ring defers diagonal blocks in any XCD group.
+bool defers_diagonals(int B, int N, int xcds, int slots)
+{
+    const int nb = (N + kPCT - 1) / kPCT;
+    for (int g = 0; g < xcds; ++g)
+        if (deferred_diagonals((B - g + xcds - 1) / xcds, nb, slots) > 0) return true;
+    return false;
+}
+
 template <class S, int WC, int WQ, int MT, int NT, bool SYM>
 void launch_persistent(const void* x, const int32_t* x_off, int B, int N, int D, int T, int xcds, int groups,
                        float* pv, int32_t* pi, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
     const uint8_t* xb = static_cast<const uint8_t*>(x);
-    if (((long)D * S::kBytes) % kPCB2 == 0)
+    if (((long)D * S::kBytes) % kPCB2 == 0) {
+        // The symmetric schedule's deferred diagonal blocks, as half blocks, in a second launch
+        // (one item per slot); the timing events then span both.
+        const bool halves = SYM && defers_diagonals(B, N, xcds, groups / xcds);
         hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB2, 2, SYM>), dim3(groups),
-                              dim3(WC * WQ * kWave), 0, stream, start, stop, 0, xb, x_off, B, N, D, T, xcds,
-                              groups / xcds, pv, pi);
-    else
+                              dim3(WC * WQ * kWave), 0, stream, start, halves ? nullptr : stop, 0, xb, x_off, B, N,
+                              D, T, xcds, groups / xcds, pv, pi);
+        if constexpr (SYM) {
+            if (halves)
+                hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT / 2, kPCB2, 2, false, true>),
+                                      dim3(groups), dim3(WC * WQ * kWave), 0, stream, nullptr, stop, 0, xb, x_off, B,
+                                      N, D, T, xcds, groups / xcds, pv, pi);
+        }
+    } else
         hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB, 4, SYM>), dim3(groups),
                               dim3(WC * WQ * kWave), 0, stream, start, stop, 0, xb, x_off, B, N, D, T, xcds,
                               groups / xcds, pv, pi);

@@ -447,11 +447,30 @@ def _sym_case(name, dtype):
     if name == "packed_ragged":
         ns = [1, 256, 257, 512, 513, 1000, 3, 700]
         return [store(clustered(rng, n, 64, k=25), dtype) for n in ns], 1000, 64
+    if name == "deferred_diagonals":
+        # 90 images on 8 XCD groups of 32 slots: groups of 12 images (120 blocks) take whole
+        # rounds only with a last round of 24; groups of 11 (110 blocks) defer 14 diagonal
+        # blocks (all of 3 images', 2 of a fourth) to the half-block second launch.
+        return [store(clustered(rng, 1024, 64, k=25), dtype) for _ in range(90)], 1024, 64
+    if name == "deferred_packed":
+        # 88 ragged images (deferred half blocks past an image's end are skipped), every
+        # fourth one made of duplicated rows (exact ties inside the half blocks).
+        sizes = [1024, 1000, 769, 768, 513, 256, 1, 900]
+        imgs = []
+        for b in range(88):
+            n = sizes[b % len(sizes)]
+            if b % 4 == 3 and n > 1:
+                h = clustered(rng, (n + 1) // 2, 64, k=20)
+                imgs.append(store(np.repeat(h, 2, axis=0)[:n], dtype))
+            else:
+                imgs.append(store(clustered(rng, n, 64, k=25), dtype))
+        return imgs, 1024, 64
     raise KeyError(name)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("name", ["dense_777", "rows_192_bytes", "duplicated_rows", "all_equal", "packed_ragged"])
+@pytest.mark.parametrize("name", ["dense_777", "rows_192_bytes", "duplicated_rows", "all_equal", "packed_ragged",
+                                  "deferred_diagonals", "deferred_packed"])
 def test_symmetric_schedule_partials_bit_identical(dtype, name):
     """The symmetric schedule (blocks on and above the diagonal, each off-diagonal
     block's argmax taken in both directions) must reproduce the full schedule's
@@ -461,7 +480,7 @@ def test_symmetric_schedule_partials_bit_identical(dtype, name):
     ns = [r.shape[0] for r in rows]
     B = len(rows)
     print(f"symmetric partials {name} {dtype} ns={ns} D={D}", flush=True)
-    packed = name == "packed_ragged"
+    packed = name in ("packed_ragged", "deferred_packed")
     if packed:
         x2 = torch.cat(rows).to(DEV)
         x_off = torch.from_numpy(np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)).to(DEV)
