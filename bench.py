@@ -33,8 +33,8 @@ AFF_SAMPLE = 8   # every 8th timed step carries the affinity kernels' timing eve
 # defers diagonal blocks, the half-block launch) from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "111a37e1c9290d6de885502254835c5648ac9c6fd77f1bfb04ac80a4229b50a2",
-           "bytes_per_launch": 149372361}
+TRAFFIC = {"source_sha256": "563cab8cb96975ea8311272956ec1c480cfa404c2d86e9c5debb740de35eb22f",
+           "bytes_per_launch": 149268217}
 
 
 def log(*a):
