@@ -6,8 +6,11 @@
 // lanes busy and every global access is a 16-byte, fully coalesced load or
 // store. A lane loads a small batch of vectors before storing any, so several
 // loads per lane are in flight (one load then one store per lane left the
-// gather latency-bound). Output rows are written once and never re-read by the
-// kernel, so they are stored with non-temporal hints.
+// gather latency-bound). The merged rows of the pair average are stored plainly:
+// the next insertion's affinity and average, or the gather, read them right
+// after, and a plain store leaves them in the last-level cache. The gather's
+// full token grid is read by nothing after it and is stored with non-temporal
+// hints.
 #include "mpm_device.h"
 #include "mpm_launch.h"
 
@@ -105,7 +108,7 @@ __global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
             if (ib != ia) out = mean16(va, load16(ximg + ib * rowbytes + c * 16), S{});
             return out;
         },
-        [&](long k, int c, u32x4 out) { store16_stream(yimg + k * rowbytes + c * 16, out); });
+        [&](long k, int c, u32x4 out) { store16(yimg + k * rowbytes + c * 16, out); });
 }
 
 __global__ __launch_bounds__(kRowThreads) void compose_kernel(const int32_t* map_a,
