@@ -142,6 +142,23 @@ int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N
                        size_t ws_bytes, void* start_event, void* stop_event, void* stream);
 
 /*
+ * mpm_affinity with the inverse row norms of Eq. 1 given instead of computed:
+ * x_inv[r] = 1 / max(||x_r||, 1e-12) for every row r of x (device, float32,
+ * packed like x: row x_off[b] + i, or b*N + i when x_off is NULL; rows past an
+ * image's end are not read). The kernels then skip the sums of squares they
+ * otherwise take of every block they stream, about a tenth of their time; the
+ * scores are the same function of x and x_inv. For the rows that
+ * mpm_pair_average_inv wrote together with their inverse norms (a later
+ * insertion, Sec. 3.3). start_event / stop_event as in mpm_affinity_timed (may
+ * be NULL). Bfloat16 rows whose byte length is a multiple of 64 only: float32
+ * rows and other lengths return MPM_ERR_UNSUPPORTED (their kernels sum their
+ * own norms); a NULL or misaligned x_inv returns MPM_ERR_INVALID_ARG;
+ * otherwise as mpm_affinity.
+ */
+int mpm_affinity_inv(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D,
+                     int32_t dt, void* ws, size_t ws_bytes, void* start_event, void* stop_event, void* stream);
+
+/*
  * Work schedule of the affinity kernel, for tuning and testing; results do not
  * depend on it (the partials are bit-identical, and so are the nearest
  * neighbours reduced from them). The affinity of an image is symmetric
@@ -221,6 +238,18 @@ int mpm_pair_compact_ws(const int32_t* x_off, int32_t B, int32_t N, int32_t D, i
 int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count,
                      int32_t B, int32_t N, int32_t D, int32_t dt,
                      void* y, int32_t* y_off, void* stream);
+
+/*
+ * mpm_pair_average that also writes y_inv[y_off[b] + k] = 1 / max(||y_k||, 1e-12)
+ * for every merged row (device, float32, room for as many rows as y), from the
+ * stored values of y in float32, summed in a fixed order (the same result on
+ * every run). These are the x_inv that mpm_affinity_inv takes for y as the
+ * next insertion's input. Errors as mpm_pair_average; a NULL or misaligned
+ * y_inv returns MPM_ERR_INVALID_ARG.
+ */
+int mpm_pair_average_inv(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count,
+                         int32_t B, int32_t N, int32_t D, int32_t dt, void* y, int32_t* y_off, float* y_inv,
+                         void* stream);
 
 /*
  * One MPM insertion (Alg. 1) = mpm_affinity, mpm_pair_compact_ws and

@@ -40,12 +40,14 @@ SIGNATURES = {
     "mpm_workspace_offsets": (ctypes.c_int, [_i32, _i32, _szp, _szp, _szp, _szp, _szp]),
     "mpm_affinity": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp]),
     "mpm_affinity_timed": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp, _vp, _vp]),
+    "mpm_affinity_inv": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp, _vp, _vp]),
     "mpm_set_affinity_schedule": (ctypes.c_int, [_i32]),
     "mpm_affinity_schedule_used": (ctypes.c_int, [_i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_int32)]),
     "mpm_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "mpm_pair_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
     "mpm_pair_compact_ws": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
     "mpm_pair_average": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp]),
+    "mpm_pair_average_inv": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
     "mpm_merge": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
     "mpm_compose": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp, _vp]),
     "mpm_compose_unmerge": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),

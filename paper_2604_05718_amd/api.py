@@ -29,6 +29,11 @@ def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
+def c_event(ev):
+    """The hipEvent_t handle of a torch.cuda.Event that has been recorded once."""
+    return ctypes.c_void_p(ev.cuda_event)
+
+
 def _dt(x: torch.Tensor) -> int:
     try:
         return _DTYPES[x.dtype]
@@ -88,15 +93,21 @@ def pair_compact(nb, x_off=None):
     return m, src, count
 
 
-def pair_average(x, src, count, x_off=None, N=None):
-    """(y [B*N, D] packed at capacity, y_off [B+1]) cluster means."""
+def pair_average(x, src, count, x_off=None, N=None, with_inv=False):
+    """(y [B*N, D] packed at capacity, y_off [B+1]) cluster means; with ``with_inv``
+    also y_inv [B*N] float32, the inverse norms of the merged rows."""
     x2, B, N, D = _rows(x, N, x_off)
     y = torch.empty((B * N, D), dtype=x.dtype, device=x.device)
     y_off = torch.empty((B + 1,), dtype=torch.int32, device=x.device)
     lib = _lib.load()
-    _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(x2), _p(x_off), _p(src), _p(count), B, N, D, _dt(x),
-                                                        _p(y), _p(y_off), _stream()))
-    return y, y_off
+    if not with_inv:
+        _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(x2), _p(x_off), _p(src), _p(count), B, N, D, _dt(x),
+                                                            _p(y), _p(y_off), _stream()))
+        return y, y_off
+    y_inv = torch.empty((B * N,), dtype=torch.float32, device=x.device)
+    _lib.check("mpm_pair_average_inv", lib.mpm_pair_average_inv(_p(x2), _p(x_off), _p(src), _p(count), B, N, D,
+                                                                _dt(x), _p(y), _p(y_off), _p(y_inv), _stream()))
+    return y, y_off, y_inv
 
 
 def workspace_bytes(B: int, N: int) -> int:
@@ -135,6 +146,7 @@ class Merged:
     ws: torch.Tensor      # workspace; nb lives at its start
     B: int
     N: int
+    y_inv: torch.Tensor | None = None  # [B*N] float32 inverse norms of the rows of y, when asked for
 
     @property
     def nb(self) -> torch.Tensor:
@@ -153,6 +165,42 @@ def merge(x, x_off=None, N=None, ws=None) -> Merged:
     _lib.check("mpm_merge", lib.mpm_merge(_p(x2), _p(x_off), B, N, D, _dt(x), _p(y), _p(y_off), _p(m), _p(ws),
                                           ws.numel(), _stream()))
     return Merged(y, y_off, m, ws, B, N)
+
+
+def takes_norms(D: int, dtype: torch.dtype) -> bool:
+    """Whether mpm_affinity_inv accepts rows of D values of this dtype (bfloat16 rows
+    a whole number of 64 bytes)."""
+    return dtype == torch.bfloat16 and (2 * D) % 64 == 0
+
+
+def insertion(x, x_off=None, N=None, x_inv=None, want_inv=False, ws=None) -> Merged:
+    """One MPM insertion (Alg. 1) through the step entry points: affinity (with the
+    given inverse norms x_inv of the rows of x, if any), compaction from the
+    workspace partials, pair average (also writing the inverse norms of the merged
+    rows when want_inv). Equal to merge() when x_inv is None."""
+    x2, B, N, D = _rows(x, N, x_off)
+    dev = x.device
+    ws = _workspace(B, N, dev, ws)
+    y = torch.empty((B * N, D), dtype=x.dtype, device=dev)
+    y_off = torch.empty((B + 1,), dtype=torch.int32, device=dev)
+    m = torch.empty((B, N), dtype=torch.int32, device=dev)
+    y_inv = torch.empty((B * N,), dtype=torch.float32, device=dev) if want_inv else None
+    lib, st, dt, n = _lib.load(), _stream(), _dt(x), ws.numel()
+    if x_inv is None:
+        _lib.check("mpm_affinity", lib.mpm_affinity(_p(x2), _p(x_off), B, N, D, dt, _p(ws), n, st))
+    else:
+        _lib.check("mpm_affinity_inv", lib.mpm_affinity_inv(_p(x2), _p(x_off), _p(x_inv), B, N, D, dt, _p(ws), n,
+                                                            None, None, st))
+    _lib.check("mpm_pair_compact_ws", lib.mpm_pair_compact_ws(_p(x_off), B, N, D, dt, _p(m), _p(ws), n, st))
+    off = _lib.workspace_offsets(B, N)
+    src, count = _p(ws[off["src"]:]), _p(ws[off["count"]:])
+    if y_inv is None:
+        _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(x2), _p(x_off), src, count, B, N, D, dt, _p(y),
+                                                            _p(y_off), st))
+    else:
+        _lib.check("mpm_pair_average_inv", lib.mpm_pair_average_inv(_p(x2), _p(x_off), src, count, B, N, D, dt,
+                                                                    _p(y), _p(y_off), _p(y_inv), st))
+    return Merged(y, y_off, m, ws, B, N, y_inv)
 
 
 def compose(map_a, map_b, out=None):
@@ -207,17 +255,20 @@ class ScheduleResult:
 
 def run_schedule(x, insertions: int = 2, workspaces=None) -> ScheduleResult:
     """Insertions with identity blocks in between (Sec. 3.3), composed maps
-    (Eq. 3) and one gather back to the full grid (Eq. 4)."""
+    (Eq. 3) and one gather back to the full grid (Eq. 4). Each insertion after the
+    first takes the inverse norms of its input rows from the pair average that
+    wrote them (rows a whole number of 64 bytes), as Schedule does."""
     B, N, D = x.shape
+    norms = takes_norms(D, x.dtype)
     stages = []
-    cur, cur_off = x, None
+    cur, cur_off, cur_inv = x, None, None
     rstar = None
     for s in range(insertions):
         ws = None if workspaces is None else workspaces[s]
-        m = merge(cur, cur_off, N=N, ws=ws)
+        m = insertion(cur, cur_off, N=N, x_inv=cur_inv, want_inv=norms and s + 1 < insertions, ws=ws)
         stages.append(m)
         rstar = m.map if rstar is None else compose(rstar, m.map)
-        cur, cur_off = m.y, m.y_off
+        cur, cur_off, cur_inv = m.y, m.y_off, m.y_inv
     out = unmerge(cur, cur_off, rstar)
     return ScheduleResult(stages, rstar, out)
 
@@ -255,6 +306,10 @@ class Schedule:
         self.map = [torch.empty((B, N), **i32) for _ in range(insertions)]
         self.y = [torch.empty((B * N, D), dtype=dtype, device=dev) for _ in range(insertions)]
         self.y_off = [torch.empty((B + 1,), **i32) for _ in range(insertions)]
+        # Inverse norms of each insertion's merged rows, for the next insertion's affinity.
+        norms = takes_norms(D, dtype)
+        self.y_inv = [torch.empty((B * N,), dtype=torch.float32, device=dev) if norms and s + 1 < insertions
+                      else None for s in range(insertions)]
         # With one insertion the map is the composed map: the gather reads it directly.
         self.rstar = self.map[0] if insertions == 1 else torch.empty((B, N), **i32)
         self.rchain = torch.empty((B, N), **i32) if insertions > 2 else None  # maps composed before the last
@@ -287,25 +342,32 @@ class Schedule:
                 marks[k].record()
             k += 1
 
-        cur, cur_off = x, None
+        cur, cur_off, cur_inv = x, None, None
         for s in range(self.insertions):
             ws = self.ws[s]
             mark()
-            if affinity_events is None:
+            ev0, ev1 = (None, None) if affinity_events is None else (c_event(e) for e in affinity_events[s])
+            if cur_inv is not None:
+                _lib.check("mpm_affinity_inv", lib.mpm_affinity_inv(_p(cur), _p(cur_off), _p(cur_inv), B, N, D, dt,
+                                                                    _p(ws), ws.numel(), ev0, ev1, st))
+            elif affinity_events is None:
                 _lib.check("mpm_affinity", lib.mpm_affinity(_p(cur), _p(cur_off), B, N, D, dt, _p(ws), ws.numel(), st))
             else:
-                ev0, ev1 = affinity_events[s]
                 _lib.check("mpm_affinity_timed", lib.mpm_affinity_timed(_p(cur), _p(cur_off), B, N, D, dt, _p(ws),
-                                                                        ws.numel(), ev0.cuda_event, ev1.cuda_event,
-                                                                        st))
+                                                                        ws.numel(), ev0, ev1, st))
             mark()
             _lib.check("mpm_pair_compact_ws", lib.mpm_pair_compact_ws(_p(cur_off), B, N, D, dt, _p(self.map[s]),
                                                                       _p(ws), ws.numel(), st))
             mark()
-            _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(cur), _p(cur_off), _p(self.src[s]),
-                                                                _p(self.count[s]), B, N, D, dt, _p(self.y[s]),
-                                                                _p(self.y_off[s]), st))
-            cur, cur_off = self.y[s], self.y_off[s]
+            if self.y_inv[s] is None:
+                _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(cur), _p(cur_off), _p(self.src[s]),
+                                                                    _p(self.count[s]), B, N, D, dt, _p(self.y[s]),
+                                                                    _p(self.y_off[s]), st))
+            else:
+                _lib.check("mpm_pair_average_inv", lib.mpm_pair_average_inv(
+                    _p(cur), _p(cur_off), _p(self.src[s]), _p(self.count[s]), B, N, D, dt, _p(self.y[s]),
+                    _p(self.y_off[s]), _p(self.y_inv[s]), st))
+            cur, cur_off, cur_inv = self.y[s], self.y_off[s], self.y_inv[s]
         if self.insertions == 1:
             mark()
             _lib.check("mpm_unmerge", lib.mpm_unmerge(_p(cur), _p(cur_off), _p(self.rstar), None, 0, B, N, D, dt,

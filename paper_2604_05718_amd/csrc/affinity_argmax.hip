@@ -427,10 +427,17 @@ __host__ __device__ inline int deferred_diagonals(int nimg, int nb, int slots)
 // 256 candidates and one half of its queries (QT = CT/2). A diagonal block needs no
 // reverse direction, so the two halves write disjoint query partials, and each score
 // comes from the same MFMA sequence as in a whole block.
+//
+// xinv (may be null): the inverse row norms 1 / max(||x_j||, 1e-12), one float per row
+// packed like x, given instead of summed from the fragments in the K loop (vector ALU
+// work in the K loop adds to its time about one for one, and these sums are a tenth of
+// it). A run-time choice in one kernel, not a second build: the two insertions of a
+// schedule then run the same code, which a second build would evict from the
+// instruction cache at every switch (that cost 3-4% of the other insertion's launch).
 template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES, bool SYM, bool HALVES = false>
 __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  // 2 waves per SIMD
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int T, int xcds,
-    int slots, float* __restrict__ pv, int32_t* __restrict__ pi)
+    int slots, float* __restrict__ pv, int32_t* __restrict__ pi, const float* __restrict__ xinv)
 {
     constexpr int THREADS = WC * WQ * kWave;
     constexpr int WAVES = WC * WQ;
@@ -458,6 +465,9 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     __shared__ float red_cv[SYM ? WQ : 1][SYM ? CT : 1];
     __shared__ int32_t red_ci[SYM ? WQ : 1][SYM ? CT : 1];
     static_assert(!SYM || QT == CT, "the symmetric schedule pairs equal blocks");
+    static_assert(CT + (SYM ? QT : 0) <= THREADS, "one given inverse norm per thread and item");
+    // Uniform. Bfloat16 rows only: the float32 kernels would spill a register with it.
+    const bool given = S::kBytes == 2 && xinv != nullptr;
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
@@ -659,13 +669,13 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                 Mfma<S>::mma(acc[mt][nt], fa[mt], fq[nt]);
             }
             // Candidate norms: m-tile mt is summed by the wave with wq == mt % WQ only.
-            if (mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(fa[mt], ss[mt]);
+            if (!given && mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(fa[mt], ss[mt]);
         }
         if constexpr (SYM) {
             // Query norms, for the reverse direction: n-tile nt is summed by the wave with wc == nt % WC.
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt)
-                if (nt % WC == wc) sq[nt] = Mfma<S>::sumsq(fq[nt], sq[nt]);
+                if (!given && nt % WC == wc) sq[nt] = Mfma<S>::sumsq(fq[nt], sq[nt]);
         }
     };
     // vmcnt(n) with expcnt and lgkmcnt unconstrained.
@@ -684,6 +694,18 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     }
 
     Item ci = find(slot);  // compute cursor
+    // With given norms, thread t fetches the inverse norm of candidate row t (t < CT) or
+    // query row t - CT (symmetric schedule) of the compute cursor's item when the cursor
+    // reaches it; the value is written to LDS at the item's end. Rows past the image are
+    // clamped, as the loads are.
+    float inv_pre = 0.0f;
+    auto fetch_inv = [&](const Item& it) {
+        if (given && it.k < nitems) {
+            const int r = tid < CT ? it.cbase + tid : it.qbase + tid - CT;
+            if (tid < CT || (SYM && tid < CT + QT)) inv_pre = xinv[it.row0 + min(r, it.n - 1)];
+        }
+    };
+    fetch_inv(ci);
     int cchunk = 0;
     int consumed = 0;
     while (ci.k < nitems) {
@@ -723,20 +745,25 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         if (++cchunk < nchunks) continue;
 
         // ---- end of an item: norms, scores, per-query partial argmax ----
+        if (given) {
+            if (tid < CT) inv_c[tid] = inv_pre;
+            else if (SYM && tid < CT + QT) inv_q[SYM ? tid - CT : 0] = inv_pre;
+        } else {
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            if (mt % WQ != wq) continue;
-            const float t = ss[mt] + __shfl_xor(ss[mt], 32);  // lanes l, l+32: the two k halves
-            ss[mt] = 0.0f;
-            if (khalf == 0) inv_c[wc * MT * 32 + mt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
-        }
-        if constexpr (SYM) {
+            for (int mt = 0; mt < MT; ++mt) {
+                if (mt % WQ != wq) continue;
+                const float t = ss[mt] + __shfl_xor(ss[mt], 32);  // lanes l, l+32: the two k halves
+                ss[mt] = 0.0f;
+                if (khalf == 0) inv_c[wc * MT * 32 + mt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+            }
+            if constexpr (SYM) {
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt) {
-                if (nt % WC != wc) continue;
-                const float t = sq[nt] + __shfl_xor(sq[nt], 32);
-                sq[nt] = 0.0f;
-                if (khalf == 0) inv_q[wq * NT * 32 + nt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+                for (int nt = 0; nt < NT; ++nt) {
+                    if (nt % WC != wc) continue;
+                    const float t = sq[nt] + __shfl_xor(sq[nt], 32);
+                    sq[nt] = 0.0f;
+                    if (khalf == 0) inv_q[wq * NT * 32 + nt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+                }
             }
         }
         lds_barrier();
@@ -963,6 +990,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         }
         cchunk = 0;
         ci = find(ci.k + slots);
+        fetch_inv(ci);
         if constexpr (HALVES) lq_off = (ci.qbase - ci.cbase + wq * NT * 32 + lrow) * CB;
     }
 }
@@ -993,6 +1021,12 @@ std::atomic<int> g_schedule{kScheduleAuto};
 
 bool use_persistent(int D, int dt) { return ((long)D * (dt == kBf16 ? 2 : 4)) % kPCB == 0; }
 
+}  // namespace
+
+bool affinity_takes_norms(int D, int dt) { return dt == kBf16 && use_persistent(D, dt); }
+
+namespace {
+
 int device_cus()
 {
     int dev = 0, cus = 0;
@@ -1011,8 +1045,8 @@ bool defers_diagonals(int B, int N, int xcds, int slots)
 }
 
 template <class S, int WC, int WQ, int MT, int NT, bool SYM>
-void launch_persistent(const void* x, const int32_t* x_off, int B, int N, int D, int T, int xcds, int groups,
-                       float* pv, int32_t* pi, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
+void launch_persistent(const void* x, const int32_t* x_off, const float* xinv, int B, int N, int D, int T, int xcds,
+                       int groups, float* pv, int32_t* pi, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
 {
     const uint8_t* xb = static_cast<const uint8_t*>(x);
     if (((long)D * S::kBytes) % kPCB2 == 0) {
@@ -1021,17 +1055,17 @@ void launch_persistent(const void* x, const int32_t* x_off, int B, int N, int D,
         const bool halves = SYM && defers_diagonals(B, N, xcds, groups / xcds);
         hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB2, 2, SYM>), dim3(groups),
                               dim3(WC * WQ * kWave), 0, stream, start, halves ? nullptr : stop, 0, xb, x_off, B, N,
-                              D, T, xcds, groups / xcds, pv, pi);
+                              D, T, xcds, groups / xcds, pv, pi, xinv);
         if constexpr (SYM) {
             if (halves)
                 hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT / 2, kPCB2, 2, false, true>),
                                       dim3(groups), dim3(WC * WQ * kWave), 0, stream, nullptr, stop, 0, xb, x_off, B,
-                                      N, D, T, xcds, groups / xcds, pv, pi);
+                                      N, D, T, xcds, groups / xcds, pv, pi, xinv);
         }
     } else
         hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB, 4, SYM>), dim3(groups),
                               dim3(WC * WQ * kWave), 0, stream, start, stop, 0, xb, x_off, B, N, D, T, xcds,
-                              groups / xcds, pv, pi);
+                              groups / xcds, pv, pi, xinv);
 }
 
 template <class S, int WC, int WQ, int MT, int NT, int CHUNK>
@@ -1105,9 +1139,10 @@ hipError_t affinity_schedule(int B, int N, int D, int dt, int* schedule)
 }
 
 hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, int D, int dt, float* pv, int32_t* pi,
-                           hipStream_t stream, hipEvent_t start, hipEvent_t stop)
+                           hipStream_t stream, hipEvent_t start, hipEvent_t stop, const float* xinv)
 {
     const int T = partial_tiles(N);
+    if (xinv && !affinity_takes_norms(D, dt)) return hipErrorInvalidValue;  // those kernels sum their own norms
     if (use_persistent(D, dt)) {
         const int cus = device_cus();
         if (cus <= 0) return hipErrorInvalidDevice;
@@ -1117,27 +1152,27 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
         const int groups = cus * kPWGS;
         if (small_blocks(B, N)) {
             if (dt == kBf16)
-                launch_persistent<Bf16, kTWC, kTWQ, kTMT, kTNT, false>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                launch_persistent<Bf16, kTWC, kTWQ, kTMT, kTNT, false>(x, x_off, xinv, B, N, D, T, xcds, groups, pv, pi,
                                                                         stream, start, stop);
             else
-                launch_persistent<F32, kTWC, kTWQ, kTMT, kTNT, false>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                launch_persistent<F32, kTWC, kTWQ, kTMT, kTNT, false>(x, x_off, xinv, B, N, D, T, xcds, groups, pv, pi,
                                                                        stream, start, stop);
             return hipGetLastError();
         }
         const bool sym = symmetric_schedule(B, N, xcds, groups / xcds);
         if (dt == kBf16) {
             if (sym)
-                launch_persistent<Bf16, kSWC, kSWQ, kSMT, kSNT, true>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                launch_persistent<Bf16, kSWC, kSWQ, kSMT, kSNT, true>(x, x_off, xinv, B, N, D, T, xcds, groups, pv, pi,
                                                                        stream, start, stop);
             else
-                launch_persistent<Bf16, kPWC, kPWQ, kPMT, kPNT, false>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                launch_persistent<Bf16, kPWC, kPWQ, kPMT, kPNT, false>(x, x_off, xinv, B, N, D, T, xcds, groups, pv, pi,
                                                                         stream, start, stop);
         } else {
             if (sym)
-                launch_persistent<F32, kSWC, kSWQ, kSMT, kSNT, true>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                launch_persistent<F32, kSWC, kSWQ, kSMT, kSNT, true>(x, x_off, xinv, B, N, D, T, xcds, groups, pv, pi,
                                                                       stream, start, stop);
             else
-                launch_persistent<F32, kPWC, kPWQ, kPMT, kPNT, false>(x, x_off, B, N, D, T, xcds, groups, pv, pi,
+                launch_persistent<F32, kPWC, kPWQ, kPMT, kPNT, false>(x, x_off, xinv, B, N, D, T, xcds, groups, pv, pi,
                                                                        stream, start, stop);
         }
         return hipGetLastError();

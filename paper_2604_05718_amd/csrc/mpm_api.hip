@@ -172,6 +172,20 @@ int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N
                                            static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event)));
 }
 
+int mpm_affinity_inv(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D,
+                     int32_t dt, void* ws, size_t ws_bytes, void* start_event, void* stop_event, void* stream)
+{
+    int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(x_inv)) return MPM_ERR_INVALID_ARG;
+    if (!mpm::affinity_takes_norms(D, dt)) return MPM_ERR_UNSUPPORTED;
+    Workspace w;
+    if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
+    return hip_status(mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, as_stream(stream),
+                                           static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event),
+                                           x_inv));
+}
+
 int mpm_set_affinity_schedule(int32_t mode) { return mpm::set_affinity_schedule(mode); }
 
 int mpm_affinity_schedule_used(int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* schedule)
@@ -230,6 +244,18 @@ int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, co
         !ok_int_ptr(y_off))
         return MPM_ERR_INVALID_ARG;
     return hip_status(mpm::launch_pair_average(x, x_off, src, count, B, N, D, dt, y, y_off, as_stream(stream)));
+}
+
+int mpm_pair_average_inv(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count, int32_t B,
+                         int32_t N, int32_t D, int32_t dt, void* y, int32_t* y_off, float* y_inv, void* stream)
+{
+    const int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(src) || !ok_int_ptr(count) || !ok_rows_ptr(y) ||
+        !ok_int_ptr(y_off) || !ok_int_ptr(y_inv))
+        return MPM_ERR_INVALID_ARG;
+    return hip_status(
+        mpm::launch_pair_average(x, x_off, src, count, B, N, D, dt, y, y_off, as_stream(stream), y_inv));
 }
 
 int mpm_merge(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* y,

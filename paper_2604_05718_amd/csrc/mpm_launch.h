@@ -10,9 +10,16 @@ namespace mpm {
 enum Dtype : int { kF32 = 0, kBf16 = 1 };
 
 // Affinity + per-candidate-tile argmax partials: pv/pi are [B][partial_tiles(N)][N].
-// start/stop (may be null) are bound to the kernel's own dispatch (hipExtLaunchKernel).
+// start/stop (may be null) are bound to the first and last of its dispatches (hipExtLaunchKernel).
+// xinv (may be null): given inverse row norms, one float per row of x (packed like x); the
+// kernels then do not sum the norms themselves. Only where affinity_takes_norms(D, dt)
+// (hipErrorInvalidValue otherwise).
 hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, int D, int dt, float* pv,
-                           int32_t* pi, hipStream_t stream, hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
+                           int32_t* pi, hipStream_t stream, hipEvent_t start = nullptr, hipEvent_t stop = nullptr,
+                           const float* xinv = nullptr);
+// Whether launch_affinity takes given inverse norms for rows of D values of dtype dt
+// (bfloat16 rows a whole number of 64 bytes: the persistent kernels).
+bool affinity_takes_norms(int D, int dt);
 // Partial slots per token in the workspace (the tile stride of pv/pi): ceil(N / 64).
 int partial_tiles(int N);
 // Candidate rows covered by one partial of the kernel launch_affinity picks for B images.
@@ -35,9 +42,10 @@ hipError_t launch_pair_compact_partials(const float* pv, const int32_t* pi, int 
 hipError_t launch_pair_compact(const int32_t* nb, const int32_t* x_off, int B, int N,
                                int32_t* map, int32_t* src, int32_t* count, hipStream_t stream);
 
+// y_inv (may be null) receives 1 / max(||y_k||, 1e-12) of every merged row k, packed like y.
 hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_t* src,
                                const int32_t* count, int B, int N, int D, int dt, void* y,
-                               int32_t* y_off, hipStream_t stream);
+                               int32_t* y_off, hipStream_t stream, float* y_inv = nullptr);
 
 hipError_t launch_compose(const int32_t* map_a, const int32_t* map_b, int B, int N,
                           int32_t* map_ab, hipStream_t stream);

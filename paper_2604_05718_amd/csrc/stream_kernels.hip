@@ -24,6 +24,7 @@ constexpr int kGatherBytesPerBlock = 16384;  // ... in the gather, which first r
 constexpr int kGatherBatch = 4;
 constexpr int kAverageBatch = 2;  // each vector of the average already loads two rows
 constexpr int kMaxRowsPerBlock = 4096;       // rows one gather workgroup resolves into LDS (16 KB)
+constexpr int kInvRowsPerBlock = 8;  // rows of one pair-average workgroup that also writes row norms
 
 // Walks the flat range [f0, f1) of 16-byte vectors of a row-major block whose rows
 // hold `vpr` vectors, U vectors per lane at a time (stride of the workgroup size):
@@ -78,6 +79,25 @@ __device__ __forceinline__ int image_offset(const int32_t* count, int b)
     return off_sh;
 }
 
+// Sum of squares of the values of one 16-byte vector, in float32.
+__device__ __forceinline__ float vec_sumsq(u32x4 v, Bf16)
+{
+    // One v_dot2c_f32_bf16 per pair of values; the words are scalars before the bit cast.
+    const uint32_t w0 = v.x, w1 = v.y, w2 = v.z, w3 = v.w;
+    float s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w0), __builtin_bit_cast(bf16x2, w0), 0.0f, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w1), __builtin_bit_cast(bf16x2, w1), s, false);
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w2), __builtin_bit_cast(bf16x2, w2), s, false);
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w3), __builtin_bit_cast(bf16x2, w3), s, false);
+}
+
+__device__ __forceinline__ float vec_sumsq(u32x4 v, F32)
+{
+    float s = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) s = fmaf(__uint_as_float(v[e]), __uint_as_float(v[e]), s);
+    return s;
+}
+
 template <class S>
 __global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, const int32_t* __restrict__ src,
@@ -109,6 +129,66 @@ __global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
             return out;
         },
         [&](long k, int c, u32x4 out) { store16(yimg + k * rowbytes + c * 16, out); });
+}
+
+// The pair average that also writes the inverse norm of every merged row, from the
+// stored values. One wave per row: lane l takes the row's vectors l, l+64, ... (a batch
+// of kAverageBatch loaded before any is stored), sums their squares in that order, and
+// a butterfly across the wave adds the lanes' sums; the order is fixed, so the result
+// is the same on every run. The merged rows are those of pair_average_kernel, bit for bit.
+template <class S>
+__global__ __launch_bounds__(kRowThreads) void pair_average_inv_kernel(
+    const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, const int32_t* __restrict__ src,
+    const int32_t* __restrict__ count, int N, int D, uint8_t* __restrict__ y, int32_t* __restrict__ y_off,
+    float* __restrict__ y_inv)
+{
+    const int b = blockIdx.y;
+    const int off = image_offset(count, b);
+    const int cnt = count[b];
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        y_off[b + 1] = off + cnt;
+        if (b == 0) y_off[0] = 0;
+    }
+    const int k0 = blockIdx.x * kInvRowsPerBlock;
+    const int k1 = min(cnt, k0 + kInvRowsPerBlock);
+    if (k0 >= k1) return;
+    const long rowbytes = (long)D * S::kBytes;
+    const int vpr = (int)(rowbytes / 16);
+    const uint8_t* ximg = x + (long)(x_off ? x_off[b] : b * N) * rowbytes;
+    uint8_t* yimg = y + (long)off * rowbytes;
+    const int32_t* srcb = src + 2L * b * N;
+    const int lane = threadIdx.x % kWave;
+    for (int k = k0 + (int)threadIdx.x / kWave; k < k1; k += kRowThreads / kWave) {
+        const int ia = srcb[2 * k];
+        const int ib = srcb[2 * k + 1];
+        const uint8_t* xa = ximg + (long)ia * rowbytes;
+        const uint8_t* xb = ximg + (long)ib * rowbytes;
+        uint8_t* yr = yimg + (long)k * rowbytes;
+        float t = 0.0f;
+        for (int c0 = lane; c0 < vpr; c0 += kWave * kAverageBatch) {
+            u32x4 v[kAverageBatch];
+#pragma unroll
+            for (int u = 0; u < kAverageBatch; ++u) {
+                const int c = c0 + u * kWave;
+                if (c < vpr) {
+                    const u32x4 va = load16(xa + c * 16);
+                    v[u] = va;  // a singleton is copied bit for bit
+                    if (ib != ia) v[u] = mean16(va, load16(xb + c * 16), S{});
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kAverageBatch; ++u) {
+                const int c = c0 + u * kWave;
+                if (c < vpr) {
+                    store16(yr + c * 16, v[u]);
+                    t += vec_sumsq(v[u], S{});
+                }
+            }
+        }
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) t += __shfl_xor(t, o);
+        if (lane == 0) y_inv[off + k] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+    }
 }
 
 __global__ __launch_bounds__(kRowThreads) void compose_kernel(const int32_t* map_a,
@@ -180,13 +260,23 @@ int rows_per_block_for(long rowbytes, long block_bytes = kRowBytesPerBlock)
 }  // namespace
 
 hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count,
-                               int B, int N, int D, int dt, void* y, int32_t* y_off, hipStream_t stream)
+                               int B, int N, int D, int dt, void* y, int32_t* y_off, hipStream_t stream, float* y_inv)
 {
     const long rowbytes = (long)D * (dt == kBf16 ? 2 : 4);
     const int rpb = rows_per_block_for(rowbytes);
     dim3 grid((N + rpb - 1) / rpb, B);
     const uint8_t* xp = static_cast<const uint8_t*>(x);
     uint8_t* yp = static_cast<uint8_t*>(y);
+    if (y_inv) {
+        const dim3 igrid((N + kInvRowsPerBlock - 1) / kInvRowsPerBlock, B);
+        if (dt == kBf16)
+            hipLaunchKernelGGL(pair_average_inv_kernel<Bf16>, igrid, dim3(kRowThreads), 0, stream, xp, x_off, src,
+                               count, N, D, yp, y_off, y_inv);
+        else
+            hipLaunchKernelGGL(pair_average_inv_kernel<F32>, igrid, dim3(kRowThreads), 0, stream, xp, x_off, src,
+                               count, N, D, yp, y_off, y_inv);
+        return hipGetLastError();
+    }
     if (dt == kBf16)
         hipLaunchKernelGGL(pair_average_kernel<Bf16>, grid, dim3(kRowThreads), 0, stream, xp, x_off, src, count, N, D,
                            rpb, yp, y_off);

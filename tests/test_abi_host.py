@@ -103,6 +103,24 @@ def test_other_entry_points_reject(lib):
     assert lib.mpm_last_hip_error() == 0
 
 
+def test_given_norm_entry_points_reject(lib):
+    """mpm_affinity_inv and mpm_pair_average_inv: the checks of their plain
+    versions, plus the norm pointer, and rows the norm-taking kernels do not cover."""
+    ws = ctypes.c_size_t(1 << 30)
+    assert lib.mpm_affinity_inv(A, None, None, 2, 8, 64, 1, A2, ws, None, None, None) == 1      # x_inv NULL
+    assert lib.mpm_affinity_inv(A, None, ctypes.c_void_p(0x10002), 2, 8, 64, 1, A2, ws, None, None, None) == 1
+    assert lib.mpm_affinity_inv(MIS, None, A, 2, 8, 64, 1, A2, ws, None, None, None) == 1       # x misaligned
+    assert lib.mpm_affinity_inv(A, None, A, 0, 8, 64, 1, A2, ws, None, None, None) == 1         # B < 1
+    assert lib.mpm_affinity_inv(A, None, A, 2, 8, 40, 1, A2, ws, None, None, None) == 2         # 80-byte rows
+    assert lib.mpm_affinity_inv(A, None, A, 2, 8, 8, 0, A2, ws, None, None, None) == 2          # 32-byte rows
+    assert lib.mpm_affinity_inv(A, None, A, 2, 8, 64, 0, A2, ws, None, None, None) == 2         # float32 rows
+    assert lib.mpm_affinity_inv(A, None, A, 2, 8, 64, 1, A2, 16, None, None, None) == 3         # workspace
+    assert lib.mpm_pair_average_inv(A, None, A, A, 2, 8, 64, 1, A2, A, None, None) == 1         # y_inv NULL
+    assert lib.mpm_pair_average_inv(A, None, A, A, 2, 8, 64, 1, MIS, A, A, None) == 1           # y misaligned
+    assert lib.mpm_pair_average_inv(A, None, A, A, 2, 8, 63, 1, A2, A, A, None) == 1            # D % 8 (bf16)
+    assert lib.mpm_last_hip_error() == 0
+
+
 def test_affinity_schedule_knob(lib):
     """Host-only: the schedule setter returns the previous mode, accepts the four
     mpm_schedule values and rejects anything else without changing the mode."""

@@ -171,6 +171,44 @@ def test_pair_average(dtype, D):
         assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("D", [8, 64, 768, 16384])
+def test_pair_average_inverse_norms(dtype, D):
+    """mpm_pair_average_inv: the same merged rows as mpm_pair_average, bit for bit,
+    and 1 / max(||y_k||, 1e-12) of every merged row against float64 norms of the
+    stored rows (float32 sums of up to 16384 squares), the same on a second run;
+    an all-zero row gives 1e12."""
+    rng = np.random.default_rng(D + 7)
+    N = 257 if D <= 768 else 40
+    ns = [N, max(1, N // 2), 1]
+    B = len(ns)
+    rows = [rng.standard_normal((n, D)) * rng.uniform(0.01, 100) for n in ns]
+    rows[1][3] = 0.0  # a zero token (its cluster is a singleton or a pair)
+    rows = [store(r, dtype) for r in rows]
+    x = torch.cat(rows).to(DEV)
+    x_off = torch.from_numpy(np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)).to(DEV)
+    nb = np.full((B, N), -1, np.int32)
+    for b, n in enumerate(ns):
+        nb[b, :n] = random_nb(rng, n)
+    nb[1, 3] = -1 if ns[1] == 1 else nb[1, 3]
+    m, src, count = mpm.pair_compact(torch.from_numpy(nb).to(DEV), x_off=x_off)
+    y, y_off = mpm.pair_average(x, src, count, x_off=x_off, N=N)
+    y2, y_off2, inv = mpm.pair_average(x, src, count, x_off=x_off, N=N, with_inv=True)
+    _, _, inv2 = mpm.pair_average(x, src, count, x_off=x_off, N=N, with_inv=True)
+    torch.cuda.synchronize()
+    total = int(y_off[B].item())
+    assert torch.equal(y_off, y_off2)
+    assert torch.equal(y[:total].view(torch.int16 if dtype == "bf16" else torch.int32),
+                       y2[:total].view(torch.int16 if dtype == "bf16" else torch.int32))
+    assert torch.equal(inv[:total].view(torch.int32), inv2[:total].view(torch.int32))
+    norm = np.sqrt((to64(y2[:total]) ** 2).sum(axis=1))
+    want = 1.0 / np.maximum(norm, 1e-12)
+    got = inv[:total].cpu().numpy().astype(np.float64)
+    zero = norm == 0
+    assert np.all(got[zero] == np.float32(1e12))
+    assert np.max(np.abs(got[~zero] / want[~zero] - 1.0)) < 2e-5
+
+
 def test_compose_and_unmerge_with_special_rows():
     rng = np.random.default_rng(9)
     B, N, D, E = 3, 50, 24, 2
@@ -513,6 +551,67 @@ def test_symmetric_schedule_partials_bit_identical(dtype, name):
         if name == "all_equal":
             assert nb[b, 0] == 1 and np.all(nb[b, 1:n] == 0)
         check_nearest(to64(rows[b]), nb[b, :n])
+
+
+def _affinity_inv_partials(x2, x_off, x_inv, B, N, D, dtype):
+    """Run mpm_affinity_inv; return the partials (pv, pi) as [B, T, N] host arrays."""
+    from paper_2604_05718_amd import _lib
+    from paper_2604_05718_amd.api import _p, _stream
+    ws = torch.empty((mpm.workspace_bytes(B, N),), dtype=torch.uint8, device=DEV)
+    dt = _lib.MPM_BF16 if dtype == "bf16" else _lib.MPM_F32
+    _lib.check("mpm_affinity_inv", _lib.load().mpm_affinity_inv(_p(x2), _p(x_off), _p(x_inv), B, N, D, dt, _p(ws),
+                                                                ws.numel(), None, None, _stream()))
+    torch.cuda.synchronize()
+    o = _lib.workspace_offsets(B, N)
+    T = (N + 63) // 64
+    pv = ws[o["pv"]:o["pv"] + 4 * B * T * N].view(torch.float32).view(B, T, N).cpu().numpy()
+    pi = ws[o["pi"]:o["pi"] + 4 * B * T * N].view(torch.int32).view(B, T, N).cpu().numpy()
+    return pv, pi
+
+
+@pytest.mark.parametrize("dtype", ["bf16"])
+@pytest.mark.parametrize("name", ["dense_777", "rows_192_bytes", "duplicated_rows", "all_equal", "packed_ragged",
+                                  "deferred_packed"])
+def test_affinity_with_given_norms(dtype, name):
+    """mpm_affinity_inv with float64-exact inverse norms (rounded to float32): the
+    full and symmetric schedules give bit-identical partials, and the nearest
+    neighbours reduced from them (larger score, then smaller index) pass the oracle
+    check, ties included."""
+    rows, N, D = _sym_case(name, dtype)
+    ns = [r.shape[0] for r in rows]
+    B = len(rows)
+    print(f"given norms {name} {dtype} B={B} D={D}", flush=True)
+    packed = name in ("packed_ragged", "deferred_packed")
+    if packed:
+        x2 = torch.cat(rows).to(DEV)
+        x_off = torch.from_numpy(np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)).to(DEV)
+        inv = np.concatenate([1.0 / np.maximum(np.sqrt((to64(r) ** 2).sum(axis=1)), 1e-12) for r in rows])
+    else:
+        x2 = torch.stack(rows).to(DEV).view(B * N, D)
+        x_off = None
+        inv = np.concatenate([1.0 / np.maximum(np.sqrt((to64(r) ** 2).sum(axis=1)), 1e-12) for r in rows])
+    x_inv = torch.from_numpy(inv.astype(np.float32)).to(DEV)
+    out = {}
+    for mode in ("full", "symmetric"):
+        prev = mpm.set_affinity_schedule(mode)
+        try:
+            out[mode] = _affinity_inv_partials(x2, x_off, x_inv, B, N, D, dtype)
+        finally:
+            mpm.set_affinity_schedule(prev)
+    (fv, fi), (sv, si) = out["full"], out["symmetric"]
+    for b, n in enumerate(ns):
+        tiles = (n + 255) // 256
+        assert np.array_equal(fv[b, :tiles, :n].view(np.uint32), sv[b, :tiles, :n].view(np.uint32)), b
+        assert np.array_equal(fi[b, :tiles, :n], si[b, :tiles, :n]), b
+        if n == 1:
+            assert fi[b, 0, 0] == -1
+            continue
+        v, i = sv[b, :tiles, :n], si[b, :tiles, :n]
+        best = v.max(axis=0)
+        nb = np.where(v == best, i, np.iinfo(np.int32).max).min(axis=0)
+        if name == "all_equal":
+            assert nb[0] == 1 and np.all(nb[1:n] == 0)
+        check_nearest(to64(rows[b]), nb)
 
 
 @pytest.mark.parametrize("schedule", ["full", "symmetric"], indirect=True)
