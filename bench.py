@@ -33,8 +33,8 @@ AFF_SAMPLE = 8   # every 8th timed step carries the affinity kernels' timing eve
 # defers diagonal blocks, the half-block launch) from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "563cab8cb96975ea8311272956ec1c480cfa404c2d86e9c5debb740de35eb22f",
-           "bytes_per_launch": 149268217}
+TRAFFIC = {"source_sha256": "7624615c1030f9fb84f11268dad733b695a69802ef7d1f68e5c3f3bc4a7bc19d",
+           "bytes_per_launch": 149961933}
 
 
 def log(*a):

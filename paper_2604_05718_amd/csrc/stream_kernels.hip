@@ -24,7 +24,16 @@ constexpr int kGatherBytesPerBlock = 16384;  // ... in the gather, which first r
 constexpr int kGatherBatch = 4;
 constexpr int kAverageBatch = 2;  // each vector of the average already loads two rows
 constexpr int kMaxRowsPerBlock = 4096;       // rows one gather workgroup resolves into LDS (16 KB)
-constexpr int kInvRowsPerBlock = 8;  // rows of one pair-average workgroup that also writes row norms
+constexpr int kInvBatch = 8;  // vectors per lane at most, in the pair average that also writes row norms
+
+// Lanes per row in the pair average that also writes row norms: a power of two, at
+// most a wave, enough for at most kInvBatch vectors per lane where a wave allows it.
+__host__ __device__ constexpr int inv_lanes(int vpr)
+{
+    int g = 1;
+    while (g < kWave && g * kInvBatch < vpr) g *= 2;
+    return g;
+}
 
 // Walks the flat range [f0, f1) of 16-byte vectors of a row-major block whose rows
 // hold `vpr` vectors, U vectors per lane at a time (stride of the workgroup size):
@@ -132,10 +141,11 @@ __global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
 }
 
 // The pair average that also writes the inverse norm of every merged row, from the
-// stored values. One wave per row: lane l takes the row's vectors l, l+64, ... (a batch
-// of kAverageBatch loaded before any is stored), sums their squares in that order, and
-// a butterfly across the wave adds the lanes' sums; the order is fixed, so the result
-// is the same on every run. The merged rows are those of pair_average_kernel, bit for bit.
+// stored values. A group of G = inv_lanes(vpr) lanes takes a row: lane j its vectors
+// j, j + G, ..., kInvBatch at a time (all loaded before any is stored), summing their
+// squares in that order; a butterfly across the group adds the lanes' sums. The order
+// is fixed, so the result is the same on every run. The merged rows are those of
+// pair_average_kernel, bit for bit.
 template <class S>
 __global__ __launch_bounds__(kRowThreads) void pair_average_inv_kernel(
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, const int32_t* __restrict__ src,
@@ -149,46 +159,46 @@ __global__ __launch_bounds__(kRowThreads) void pair_average_inv_kernel(
         y_off[b + 1] = off + cnt;
         if (b == 0) y_off[0] = 0;
     }
-    const int k0 = blockIdx.x * kInvRowsPerBlock;
-    const int k1 = min(cnt, k0 + kInvRowsPerBlock);
-    if (k0 >= k1) return;
     const long rowbytes = (long)D * S::kBytes;
     const int vpr = (int)(rowbytes / 16);
+    const int G = inv_lanes(vpr);
+    const int k0 = blockIdx.x * (kRowThreads / G);
+    if (k0 >= cnt) return;
+    const int k = k0 + (int)threadIdx.x / G;  // this group's row
+    const int j = threadIdx.x % G;
+    const bool live = k < cnt;
     const uint8_t* ximg = x + (long)(x_off ? x_off[b] : b * N) * rowbytes;
-    uint8_t* yimg = y + (long)off * rowbytes;
-    const int32_t* srcb = src + 2L * b * N;
-    const int lane = threadIdx.x % kWave;
-    for (int k = k0 + (int)threadIdx.x / kWave; k < k1; k += kRowThreads / kWave) {
-        const int ia = srcb[2 * k];
-        const int ib = srcb[2 * k + 1];
-        const uint8_t* xa = ximg + (long)ia * rowbytes;
-        const uint8_t* xb = ximg + (long)ib * rowbytes;
-        uint8_t* yr = yimg + (long)k * rowbytes;
-        float t = 0.0f;
-        for (int c0 = lane; c0 < vpr; c0 += kWave * kAverageBatch) {
-            u32x4 v[kAverageBatch];
+    int ia = 0, ib = 0;
+    if (live) {
+        ia = src[2L * b * N + 2 * k];
+        ib = src[2L * b * N + 2 * k + 1];
+    }
+    const uint8_t* xa = ximg + (long)ia * rowbytes;
+    const uint8_t* xb = ximg + (long)ib * rowbytes;
+    uint8_t* yr = y + (long)(off + k) * rowbytes;
+    float t = 0.0f;
+    for (int c0 = j; c0 < vpr; c0 += G * kInvBatch) {
+        u32x4 v[kInvBatch];
 #pragma unroll
-            for (int u = 0; u < kAverageBatch; ++u) {
-                const int c = c0 + u * kWave;
-                if (c < vpr) {
-                    const u32x4 va = load16(xa + c * 16);
-                    v[u] = va;  // a singleton is copied bit for bit
-                    if (ib != ia) v[u] = mean16(va, load16(xb + c * 16), S{});
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < kAverageBatch; ++u) {
-                const int c = c0 + u * kWave;
-                if (c < vpr) {
-                    store16(yr + c * 16, v[u]);
-                    t += vec_sumsq(v[u], S{});
-                }
+        for (int u = 0; u < kInvBatch; ++u) {
+            const int c = c0 + u * G;
+            if (live && c < vpr) {
+                const u32x4 va = load16(xa + c * 16);
+                v[u] = va;  // a singleton is copied bit for bit
+                if (ib != ia) v[u] = mean16(va, load16(xb + c * 16), S{});
             }
         }
 #pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) t += __shfl_xor(t, o);
-        if (lane == 0) y_inv[off + k] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+        for (int u = 0; u < kInvBatch; ++u) {
+            const int c = c0 + u * G;
+            if (live && c < vpr) {
+                store16(yr + c * 16, v[u]);
+                t += vec_sumsq(v[u], S{});
+            }
+        }
     }
+    for (int o = G / 2; o > 0; o >>= 1) t += __shfl_xor(t, o);
+    if (live && j == 0) y_inv[off + k] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
 }
 
 __global__ __launch_bounds__(kRowThreads) void compose_kernel(const int32_t* map_a,
@@ -268,7 +278,8 @@ hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_
     const uint8_t* xp = static_cast<const uint8_t*>(x);
     uint8_t* yp = static_cast<uint8_t*>(y);
     if (y_inv) {
-        const dim3 igrid((N + kInvRowsPerBlock - 1) / kInvRowsPerBlock, B);
+        const int rows = kRowThreads / inv_lanes((int)(rowbytes / 16));
+        const dim3 igrid((N + rows - 1) / rows, B);
         if (dt == kBf16)
             hipLaunchKernelGGL(pair_average_inv_kernel<Bf16>, igrid, dim3(kRowThreads), 0, stream, xp, x_off, src,
                                count, N, D, yp, y_off, y_inv);

@@ -172,14 +172,16 @@ def test_pair_average(dtype, D):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("D", [8, 64, 768, 16384])
+@pytest.mark.parametrize("D", [8, 64, 768, 2048, 2056, 16384])
 def test_pair_average_inverse_norms(dtype, D):
     """mpm_pair_average_inv: the same merged rows as mpm_pair_average, bit for bit,
+    on rows of 16 bytes to 64 KB (1 to 4096 vectors of 16 bytes: 1 to 64 lanes per
+    row, one or several batches of vectors per lane, a ragged last batch),
     and 1 / max(||y_k||, 1e-12) of every merged row against float64 norms of the
     stored rows (float32 sums of up to 16384 squares), the same on a second run;
     an all-zero row gives 1e12."""
     rng = np.random.default_rng(D + 7)
-    N = 257 if D <= 768 else 40
+    N = 257 if D <= 2056 else 40
     ns = [N, max(1, N // 2), 1]
     B = len(ns)
     rows = [rng.standard_normal((n, D)) * rng.uniform(0.01, 100) for n in ns]
