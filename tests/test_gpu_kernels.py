@@ -310,6 +310,33 @@ def test_schedule_small_batch_all_images():
         check_schedule_image(x[b], "bf16", res, b)
 
 
+@pytest.mark.parametrize("insertions", [3, 4])
+def test_schedule_more_insertions(insertions):
+    """Three and four insertions on a bf16 batch: every insertion after the first
+    takes the inverse norms the previous pair average wrote (including rows merged
+    from rows that were themselves merged with given norms). Every stage passes the
+    oracle check, and the preallocated Schedule equals run_schedule bit for bit."""
+    from paper_2604_05718_amd import api
+
+    rng = np.random.default_rng(30 + insertions)
+    B, N, D = 3, 700, 128
+    x = torch.stack([store(clustered(rng, N, D, k=20, sigma=0.25), "bf16") for _ in range(B)])
+    print(f"more insertions {insertions} B={B} N={N} D={D}", flush=True)
+    xd = x.to(DEV)
+    res = mpm.run_schedule(xd, insertions=insertions)
+    sched = api.Schedule(B, N, D, torch.bfloat16, insertions=insertions)
+    out = sched.run(xd)
+    torch.cuda.synchronize()
+    assert len(res.stages) == insertions
+    for b in range(B):
+        check_schedule_image(x[b], "bf16", res, b)
+    assert torch.equal(out, res.out) and torch.equal(sched.rstar, res.rstar)
+    for s in range(insertions):
+        assert torch.equal(sched.map[s], res.stages[s].map)
+        rows = int(sched.y_off[s][-1])
+        assert torch.equal(sched.y[s][:rows], res.stages[s].y[:rows])
+
+
 def test_deterministic_across_runs():
     rng = np.random.default_rng(4)
     x = torch.stack([store(clustered(rng, 1024, 256, k=30), "bf16") for _ in range(8)]).to(DEV)
