@@ -27,14 +27,12 @@ PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 matrix
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak"
-AFF_SAMPLE = 8   # every 8th timed step carries the affinity kernels' timing events
 
 # HBM traffic of one affinity step (the whole-block launch and, where the schedule
 # defers diagonal blocks, the half-block launch) from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
 # the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "7624615c1030f9fb84f11268dad733b695a69802ef7d1f68e5c3f3bc4a7bc19d",
-           "bytes_per_launch": 149961933}
+TRAFFIC = {"source_sha256": "", "bytes_per_launch": None}
 
 
 def log(*a):
@@ -66,8 +64,10 @@ def executed_affinity_flops(cfg, counts, schedule):
 
 
 def algorithmic_work(cfg, counts):
-    """Per kernel of one step: ('flops'|'bytes', amount). counts[s] = per-image
-    token counts after insertion s (counts[-1] = N for every image)."""
+    """Per kernel step of one step: ('flops'|'bytes', amount). counts[s] = per-image
+    token counts after insertion s (counts[-1] = N for every image). The affinity step
+    carries the compaction (its last workgroup per image); its work is counted as the
+    affinity's flops (the compaction's few bytes are not)."""
     s = 2 if cfg.dtype == "bf16" else 4
     D, N, B = cfg.D, cfg.N, cfg.B
     work = []
@@ -75,10 +75,8 @@ def algorithmic_work(cfg, counts):
     for st in range(cfg.insertions):
         n_out = counts[st]
         work.append(("flops", sum(2.0 * n * n * D for n in n_in)))
-        # compact: read nb (4n), write map (4N) and src (8n'), count (4)
-        work.append(("bytes", sum(4.0 * n + 4.0 * N + 8.0 * m + 4 for n, m in zip(n_in, n_out))))
-        # average: read every member row once, write every cluster row, read src
-        work.append(("bytes", sum((n + m) * D * s + 8.0 * m for n, m in zip(n_in, n_out))))
+        # average: read every member row once, write every cluster row, read src and the offsets
+        work.append(("bytes", sum((n + m) * D * s + 8.0 * m + 4 for n, m in zip(n_in, n_out))))
         n_in = n_out
     # gather: read the composed map, each final row once, write the full grid
     gather = sum(4.0 * N + m * D * s + N * D * s for m in n_in)
@@ -94,10 +92,10 @@ def algorithmic_work(cfg, counts):
     return work
 
 
-def cpu_baseline(cfg, x_cpu, budget_s: float):
+def cpu_baseline(cfg, x_cpu, budget_s: float, threads: int | None = None):
     import oracle
 
-    threads = oracle.default_threads()
+    threads = threads or oracle.default_threads()
     t0 = time.perf_counter()
     done = 0
     # Images of the batch in order, starting over after the last one, until the
@@ -141,6 +139,8 @@ def main() -> int:
                     help="budget of the CPU oracle baseline (0 skips it)")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="steps timed after evicting the caches (0 skips them)")
+    ap.add_argument("--cpu-single-seconds", type=float, default=3.0,
+                    help="budget of the single-thread CPU oracle figure (0 skips it)")
     ap.add_argument("--schedule", default="auto", choices=["auto", "full", "symmetric", "full_64"],
                     help="affinity work schedule (auto: the library's choice for the batch shape)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -171,38 +171,42 @@ def main() -> int:
     from paper_2604_05718_amd import api, synth
 
     cfg = synth.config(args.workload)
-    mpm.set_affinity_schedule(args.schedule)
     dev = torch.device("cuda:0")
     dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     log(f"bench: {cfg.name} B={cfg.B} N={cfg.N} D={cfg.D} {cfg.dtype}, generating inputs")
     x_cpu = synth.make_batch(cfg, seed=0)
     x = x_cpu.to(dev)
-    sched = api.Schedule(cfg.B, cfg.N, cfg.D, dtype, cfg.insertions)
+    sched = api.Schedule(cfg.B, cfg.N, cfg.D, dtype, cfg.insertions, schedule=args.schedule)
 
     for _ in range(args.warmup):
         sched.run(x)
     torch.cuda.synchronize()
     log(f"bench: warmup {args.warmup} done, timing {args.steps} steps")
 
-    # Timed region: K steps. The affinity kernels (the dominant kernel) of every
-    # AFF_SAMPLE-th step are timed by events bound to their own dispatches; each such
-    # event costs a few microseconds of stream time, so only a sample carries them.
-    sampled = list(range(0, args.steps, AFF_SAMPLE))
-    aff_ev = {k: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                  for _ in range(cfg.insertions)] for k in sampled}
-    for pairs in aff_ev.values():
-        for e0, e1 in pairs:  # torch creates events lazily, at their first record
-            e0.record()
-            e1.record()
+    # Timed region: K steps and nothing else on the stream between its two events.
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for k in range(args.steps):
-        sched.run(x, affinity_events=aff_ev.get(k))
+        sched.run(x)
     end.record()
     torch.cuda.synchronize()
     ms_per_step = start.elapsed_time(end) / args.steps
-    aff_ms = [sum(aff_ev[k][s][0].elapsed_time(aff_ev[k][s][1]) for k in sampled) / len(sampled)
+
+    # The dominant kernel, timed in its own loop after the timed region: events bound to
+    # the affinity launches of every step (start on the first launch, stop on the last),
+    # which add no stream commands between kernels but cost a few microseconds each.
+    aff_ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(cfg.insertions)] for _ in range(args.steps)]
+    for pairs in aff_ev:
+        for e0, e1 in pairs:  # torch creates events lazily, at their first record
+            e0.record()
+            e1.record()
+    torch.cuda.synchronize()
+    for k in range(args.steps):
+        sched.run(x, affinity_events=aff_ev[k])
+    torch.cuda.synchronize()
+    aff_ms = [sum(aff_ev[k][s][0].elapsed_time(aff_ev[k][s][1]) for k in range(args.steps)) / args.steps
               for s in range(cfg.insertions)]
     log(f"bench: {ms_per_step * 1e3:.1f} us/step, affinity kernels " + ", ".join(f"{m * 1e3:.1f}" for m in aff_ms) + " us")
 
@@ -278,7 +282,7 @@ def main() -> int:
     except Exception as exc:  # reported, not fatal: the eager figures above stand on their own
         graph = {"error": f"{type(exc).__name__}: {exc}"}
 
-    schedule = mpm.affinity_schedule_used(cfg.B, cfg.N, cfg.D, dtype)
+    schedule = mpm.affinity_schedule_used(cfg.B, cfg.N, cfg.D, dtype, args.schedule)
     executed = executed_affinity_flops(cfg, counts, schedule)
     kernels = []
     for name, ms, (kind, amount) in zip(names, per_kernel_ms, work):
@@ -287,7 +291,7 @@ def main() -> int:
             tf = amount / (ms * 1e-3) / 1e12
             peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
             ent.update({"gflop": round(amount / 1e9, 3), "tflops": round(tf, 1), "frac_mfma": round(tf / peak, 4),
-                        "executed_gflop": round(executed[int(name[len("affinity"):]) - 1] / 1e9, 3)})
+                        "executed_gflop": round(executed[int(name[len("affinity+compact"):]) - 1] / 1e9, 3)})
         else:
             gbs = amount / (ms * 1e-3) / 1e9
             ent.update({"mbytes": round(amount / 1e6, 3), "gbs": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
@@ -328,7 +332,7 @@ def main() -> int:
                                 f"{cfg.insertions} MPM insertions + compose + gather"),
                    "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "none (1 GPU)"},
         "tokens_per_s": round(value * cfg.N, 0),
-        "affinity_timed_steps": len(sampled),
+        "affinity_timed_steps": args.steps,
         "ms_per_step_with_per_kernel_events": round(ms_marked, 4),
         "survivors_mean": [round(sum(c) / len(c), 1) for c in counts],
         "roofline": roofline,
@@ -340,6 +344,9 @@ def main() -> int:
     if args.cpu_seconds > 0:
         log("bench: timing the CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(cfg, x_cpu, args.cpu_seconds)
+    if args.cpu_single_seconds > 0:
+        log("bench: timing the CPU oracle on one thread")
+        result["cpu_baseline_single_thread"] = cpu_baseline(cfg, x_cpu, args.cpu_single_seconds, threads=1)
     print(json.dumps(result), flush=True)
     return 0
 

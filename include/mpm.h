@@ -34,9 +34,12 @@
  *   b*N + i belongs to token i of image b, for i < n_b. Ids are 0-based and
  *   image-local.
  * - Ties: the argmax keeps the lowest index j among equal scores.
+ * - `schedule` (an mpm_schedule value) picks the affinity kernel's work
+ *   decomposition for that call only; results never depend on it.
  * - Argument errors are reported synchronously, before anything is launched:
  *     MPM_ERR_INVALID_ARG  null or misaligned pointer, B < 1, N < 1, D < 1,
- *                          D not a multiple of 8 (bf16) / 4 (f32), bad dtype;
+ *                          D not a multiple of 8 (bf16) / 4 (f32), bad dtype,
+ *                          unknown schedule;
  *     MPM_ERR_UNSUPPORTED  N above MPM_MAX_N, B above MPM_MAX_B, D above MPM_MAX_D;
  *     MPM_ERR_WORKSPACE    workspace smaller than mpm_workspace_bytes;
  *     MPM_ERR_HIP          a launch failed; mpm_last_hip_error() holds the
@@ -44,6 +47,7 @@
  *   Device-side faults surface at the caller's next synchronisation.
  * - Results are deterministic: the same inputs give bitwise-identical outputs.
  * - Reentrant: no mutable global state besides the per-thread last HIP error.
+ *   Calls that share a workspace must be ordered (one stream, or events).
  */
 #ifndef MPM_H
 #define MPM_H
@@ -68,10 +72,27 @@ typedef enum {
     MPM_BF16 = 1   /* bfloat16 storage, float32 accumulation */
 } mpm_dtype;
 
+/*
+ * Work schedule of the affinity kernel. The affinity of an image is symmetric
+ * (Eq. 1), so MPM_SCHEDULE_SYMMETRIC computes only the 256 x 256 blocks on and
+ * above the block diagonal and takes each off-diagonal block's argmax in both
+ * directions (about half the matrix-core work for large images, for a
+ * cross-lane reduction per block); when an XCD group's blocks would leave a
+ * last round on at most half of its workgroups (rows a whole number of
+ * 128-byte chunks), that many diagonal blocks run in a second launch as two
+ * halves of their queries each. MPM_SCHEDULE_FULL_64 computes every pair of
+ * 64 x 64 blocks, so that a small batch (a single image of 1024 tokens has 16
+ * blocks of 256 x 256 but 256 of 64 x 64) still occupies every compute unit.
+ * MPM_SCHEDULE_AUTO takes the 64 x 64 blocks when the batch has at most 32
+ * blocks of 256 x 256, else the symmetric schedule when it needs fewer work
+ * rounds on the device's compute units, else the full one. The choice applies
+ * to rows whose byte length is a multiple of 64; other rows use a kernel
+ * without one. The partials (and everything reduced from them) are
+ * bit-identical under every schedule.
+ */
 typedef enum {
-    MPM_SCHEDULE_AUTO = 0,      /* 64 x 64 blocks for small batches, else symmetric when it
-                                   needs fewer work rounds (default) */
-    MPM_SCHEDULE_FULL = 1,      /* every (query block, candidate tile) pair */
+    MPM_SCHEDULE_AUTO = 0,
+    MPM_SCHEDULE_FULL = 1,      /* every (query block, candidate tile) pair of 256 x 256 */
     MPM_SCHEDULE_SYMMETRIC = 2, /* pairs on and above the block diagonal only */
     MPM_SCHEDULE_FULL_64 = 3    /* every pair of 64 x 64 blocks (small batches) */
 } mpm_schedule;
@@ -80,7 +101,7 @@ typedef enum {
 #define MPM_MAX_B 65535   /* images per call */
 #define MPM_MAX_D 16384   /* channels per token */
 
-/* Library version string, e.g. "mpm 0.1.0 gfx950". Never NULL. */
+/* Library version string, e.g. "mpm 0.2.0 gfx950". Never NULL. */
 const char* mpm_version(void);
 
 /* Human-readable name of a status code. Never NULL. */
@@ -90,27 +111,38 @@ const char* mpm_status_string(int status);
 int mpm_last_hip_error(void);
 
 /*
- * Device workspace shared by mpm_affinity, mpm_argmax, mpm_pair_compact_ws and
+ * Device workspace of mpm_affinity, mpm_affinity_compact, mpm_argmax and
  * mpm_merge: bytes needed for a batch of B images of at most N tokens. The
- * caller allocates it (256-byte aligned) and owns it; consecutive calls on one
- * stream may reuse it. Layout, as byte offsets returned by
- * mpm_workspace_offsets (each 256-byte aligned):
- *   nb    int32[B*N]          nearest neighbour per token (slot layout);
- *   src   int32[2*B*N]        (representative, partner) per cluster;
- *   count int32[B]            clusters per image;
+ * caller allocates it (256-byte aligned) and owns it; calls ordered on one
+ * stream may reuse it, for any B and N it is large enough for. Layout, as byte
+ * offsets returned by mpm_workspace_offsets (each 256-byte aligned):
+ *   sync  int32[MPM_MAX_B + 1]  arrival counters of the fused compaction
+ *                               (always at offset 0, the same for every shape);
+ *   nb    int32[B*N]            nearest neighbour per token (slot layout);
+ *   src   int32[2*B*N]          (representative, partner) of cluster k of image
+ *                               b at 2*(b*N + k) (partner == representative for
+ *                               a singleton);
  *   pv    float[B*T*N], pi int32[B*T*N]  per-candidate-tile argmax partials,
- *                             T = ceil(N / 64) slots per token: tile t of image b
- *                             for token i at (b*T + t)*N + i; a launch fills the
- *                             first ceil(n_b / w) slots, w = the block width of
- *                             its schedule (64 or 256 tokens).
- * Returns 0 for B < 1 or N < 1.
+ *                               T = ceil(N / 64) slots per token: tile t of image b
+ *                               for token i at (b*T + t)*N + i; a launch fills the
+ *                               first ceil(n_b / w) slots, w = the block width of
+ *                               its schedule (64 or 256 tokens).
+ * The sync region must be zero before a workspace's first use by
+ * mpm_affinity_compact or mpm_merge (mpm_workspace_init); every call leaves it
+ * zero again (an interrupted call may not). Returns 0 for B < 1 or N < 1.
  */
 size_t mpm_workspace_bytes(int32_t B, int32_t N);
 
 /* Byte offsets of the workspace regions listed above; any pointer may be NULL.
  * Returns MPM_OK, or MPM_ERR_INVALID_ARG for B < 1 or N < 1. */
-int mpm_workspace_offsets(int32_t B, int32_t N, size_t* nb, size_t* src, size_t* count, size_t* pv,
-                          size_t* pi);
+int mpm_workspace_offsets(int32_t B, int32_t N, size_t* sync, size_t* nb, size_t* src, size_t* pv, size_t* pi);
+
+/*
+ * Zeroes the sync region of a workspace of ws_bytes bytes (at least the
+ * region's 256 KB) with a fill kernel on `stream` (no memset node, so it may
+ * be captured in a HIP graph). Needed once after allocating a workspace.
+ */
+int mpm_workspace_init(void* ws, size_t ws_bytes, void* stream);
 
 /*
  * Cosine affinity and its self-masked row argmax, per candidate tile (Eq. 1
@@ -121,148 +153,114 @@ int mpm_workspace_offsets(int32_t B, int32_t N, size_t* nb, size_t* src, size_t*
  * stored values (bfloat16 products are exact in float32); the N x N affinity
  * is never written to memory. Dividing by ||x_i|| too would not move the
  * argmax of row i, so it is not applied.
- * x: rows of dtype `dt`, dense or packed by x_off.
+ *   x, x_off: rows of dtype `dt`, dense or packed;
+ *   x_inv (may be NULL): the inverse row norms 1 / max(||x_r||, 1e-12), one
+ *     float per row of x (packed like x; rows past an image's end are not
+ *     read), given instead of summed in the kernel's K loop (about a tenth of
+ *     its time), as mpm_pair_average writes them for the next insertion's
+ *     input (Sec. 3.3). Bfloat16 rows whose byte length is a multiple of 64
+ *     only: other rows return MPM_ERR_UNSUPPORTED with a non-NULL x_inv;
+ *   start_event / stop_event (may be NULL): hipEvent_t the caller created
+ *     (timing enabled) and owns, bound to the kernels' own dispatches
+ *     (hipExtLaunchKernel): start to the first launch, stop to the last, so
+ *     hipEventElapsedTime(start, stop) is the step's duration on the device
+ *     without extra stream commands. The step is one launch, or two when the
+ *     symmetric schedule runs deferred diagonal blocks in a second launch.
  */
-int mpm_affinity(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* ws,
-                 size_t ws_bytes, void* stream);
+int mpm_affinity(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D,
+                 int32_t dt, int32_t schedule, void* ws, size_t ws_bytes, void* start_event, void* stop_event,
+                 void* stream);
 
 /*
- * mpm_affinity with its execution interval recorded into two events, for
- * callers that time the dominant kernel of a step (telemetry, profiling)
- * without adding stream commands between kernels. start_event / stop_event
- * are hipEvent_t the caller created (timing enabled) and owns; either may be
- * NULL. They are bound to the kernels' own dispatches (hipExtLaunchKernel):
- * start to the first launch, stop to the last. The step is one launch, or two
- * when the symmetric schedule runs its deferred diagonal blocks as half blocks
- * in a second launch (see mpm_set_affinity_schedule), so
- * hipEventElapsedTime(start, stop) is the step's duration on the device. Same
- * results, arguments and errors as mpm_affinity otherwise.
+ * One insertion's affinity step and compaction step (Sec. 3.2, Alg. 1 steps 2-6)
+ * in one call: mpm_affinity, then the compaction kernel, which reduces each
+ * image's partials to nb (larger score, then smaller index; images with more
+ * than a few candidate tiles are reduced by a separate parallel launch first),
+ * tests the pairs for mutuality, marks representatives and assigns compact ids
+ * by a left-to-right scan, one workgroup per image; the workgroup that finishes
+ * the last image (found with the arrival counter in the workspace's sync
+ * region, no waiting) turns the per-image cluster counts into offsets. Writes
+ *   map[b*N + i] = r(i) for i < n_b, -1 for n_b <= i < N;
+ *   y_off[0] = 0, y_off[b+1] = y_off[b] + n'_b (int32[B+1]);
+ *   the workspace's nb and src regions (src read by mpm_pair_average).
+ * The timing events are bound to the affinity kernel's dispatches only.
+ * Arguments as mpm_affinity otherwise; the workspace's sync region must be zero
+ * (mpm_workspace_init).
  */
-int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* ws,
-                       size_t ws_bytes, void* start_event, void* stop_event, void* stream);
-
-/*
- * mpm_affinity with the inverse row norms of Eq. 1 given instead of computed:
- * x_inv[r] = 1 / max(||x_r||, 1e-12) for every row r of x (device, float32,
- * packed like x: row x_off[b] + i, or b*N + i when x_off is NULL; rows past an
- * image's end are not read). The kernels then skip the sums of squares they
- * otherwise take of every block they stream, about a tenth of their time; the
- * scores are the same function of x and x_inv. For the rows that
- * mpm_pair_average_inv wrote together with their inverse norms (a later
- * insertion, Sec. 3.3). start_event / stop_event as in mpm_affinity_timed (may
- * be NULL). Bfloat16 rows whose byte length is a multiple of 64 only: float32
- * rows and other lengths return MPM_ERR_UNSUPPORTED (their kernels sum their
- * own norms); a NULL or misaligned x_inv returns MPM_ERR_INVALID_ARG;
- * otherwise as mpm_affinity.
- */
-int mpm_affinity_inv(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D,
-                     int32_t dt, void* ws, size_t ws_bytes, void* start_event, void* stop_event, void* stream);
-
-/*
- * Work schedule of the affinity kernel, for tuning and testing; results do not
- * depend on it (the partials are bit-identical, and so are the nearest
- * neighbours reduced from them). The affinity of an image is symmetric
- * (Eq. 1), so the symmetric schedule computes only the 256 x 256 blocks on and
- * above the block diagonal and takes each off-diagonal block's argmax in both
- * directions, about half the matrix-core work for large images at the price of
- * a cross-lane reduction per block. For rows that are a whole number of
- * 128-byte chunks, when an XCD group's blocks would leave a last round on at
- * most half of its workgroups, that many diagonal blocks are deferred to a
- * second launch that runs each as two halves of its queries, one per
- * workgroup. MPM_SCHEDULE_FULL_64 computes every pair of
- * 64 x 64 blocks, so that a small batch (a single image of 1024 tokens has 16
- * blocks of 256 x 256 but 256 of 64 x 64) still occupies every compute unit.
- * MPM_SCHEDULE_AUTO (the default) takes the 64 x 64 blocks when the batch has
- * at most 32 blocks of 256 x 256, else the symmetric schedule when it needs
- * fewer work rounds on the device's compute units, else the full one. Applies
- * to bfloat16 and float32 rows whose byte length is a multiple of 64 (other
- * rows use a kernel without a schedule choice). Process-wide: it affects every
- * later call on any thread; calls already enqueued are not changed. Returns the
- * previous mode, or -1 (changing nothing) when `mode` is not an mpm_schedule
- * value.
- */
-int mpm_set_affinity_schedule(int32_t mode);
+int mpm_affinity_compact(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D,
+                         int32_t dt, int32_t schedule, int32_t* map, int32_t* y_off, void* ws, size_t ws_bytes,
+                         void* start_event, void* stop_event, void* stream);
 
 /*
  * The schedule (MPM_SCHEDULE_FULL, MPM_SCHEDULE_SYMMETRIC or
- * MPM_SCHEDULE_FULL_64, never AUTO) that mpm_affinity would run for B images
- * of at most N tokens of D channels of dtype dt on the current device under
- * the current mode, written to *schedule (a host pointer). For reporting the
- * matrix-core work a call issues: about 2 * w^2 * D flops per w x w block,
- * nb^2 blocks per image of nb = ceil(n_b / w) blocks under the full schedules
- * (w = 256, or 64 for MPM_SCHEDULE_FULL_64) and nb (nb + 1) / 2 under the
- * symmetric one (w = 256). Rows whose byte length is not a multiple of 64
- * always report MPM_SCHEDULE_FULL. Returns MPM_OK,
- * MPM_ERR_INVALID_ARG for bad sizes or a NULL pointer, or MPM_ERR_HIP when
- * the device cannot be queried.
+ * MPM_SCHEDULE_FULL_64, never AUTO) that mpm_affinity runs for B images of at
+ * most N tokens of D channels of dtype dt under `schedule` on the current
+ * device, written to *used (a host pointer). For reporting the matrix-core
+ * work a call issues: about 2 * w^2 * D flops per w x w block, nb^2 blocks per
+ * image of nb = ceil(n_b / w) blocks under the full schedules (w = 256, or 64
+ * for MPM_SCHEDULE_FULL_64) and nb (nb + 1) / 2 under the symmetric one
+ * (w = 256). Rows whose byte length is not a multiple of 64 always report
+ * MPM_SCHEDULE_FULL. Returns MPM_OK, MPM_ERR_INVALID_ARG for bad sizes, an
+ * unknown schedule or a NULL pointer, or MPM_ERR_HIP when the device cannot be
+ * queried.
  */
-int mpm_affinity_schedule_used(int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* schedule);
+int mpm_affinity_schedule_used(int32_t B, int32_t N, int32_t D, int32_t dt, int32_t schedule, int32_t* used);
 
 /*
- * Nearest neighbours: mpm_affinity, then the reduction of the partials.
+ * Nearest neighbours: mpm_affinity (norms summed in the kernel), then the
+ * reduction of the partials.
  *   nb[b*N + i] = argmax_{j != i, j < n_b} cos(x_i, x_j), lowest j on equal
  *                 scores; -1 when n_b == 1. Entries i >= n_b are not written.
  *   best[b*N + i] (optional, may be NULL) = the float32 cosine of that pair.
  * nb and best are caller arrays (not the workspace).
  */
-int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* nb,
-               float* best, void* ws, size_t ws_bytes, void* stream);
+int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t schedule,
+               int32_t* nb, float* best, void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Mutual pairs and compact ids (Sec. 3.2, Alg. 1) from nb.
+ * Mutual pairs and compact ids (Sec. 3.2, Alg. 1) from given neighbours nb
+ * (slot layout, values in [0, n_b) or -1 for n_b == 1).
  *   map[b*N + i] = r(i) for i < n_b, -1 for n_b <= i < N;
  *   src[2*(b*N + k)], src[2*(b*N + k) + 1] = (representative, partner) of
- *     cluster k < count[b] (partner == representative for a singleton);
- *   count[b] = n'_b, the number of clusters of image b.
+ *     cluster k < n'_b (partner == representative for a singleton);
+ *   y_off[0] = 0, y_off[b+1] = y_off[b] + n'_b.
  * x_off: the offsets of the tokens nb was computed on (NULL = dense, n_b = N).
+ * Two launches (one workgroup per image, then the offsets).
  */
-int mpm_pair_compact(const int32_t* nb, const int32_t* x_off, int32_t B, int32_t N,
-                     int32_t* map, int32_t* src, int32_t* count, void* stream);
+int mpm_pair_compact(const int32_t* nb, const int32_t* x_off, int32_t B, int32_t N, int32_t* map, int32_t* src,
+                     int32_t* y_off, void* stream);
 
 /*
- * mpm_pair_compact reading the partials mpm_affinity left in the workspace
- * (D and dt must be those of that call): reduces them to nb (written to the
- * workspace's nb region), then writes map, and src/count into the workspace.
- */
-int mpm_pair_compact_ws(const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* map,
-                        void* ws, size_t ws_bytes, void* stream);
-
-/*
- * Cluster means (Eq. 2), packed.
- *   y_off[0] = 0, y_off[b+1] = y_off[b] + count[b];
+ * Cluster means (Eq. 2), packed by the offsets the compaction wrote:
  *   y[y_off[b] + k] = mean of the rows src names for cluster k of image b,
  *     computed in float32 and rounded once (nearest even) to `dt`; a
- *     singleton is copied bit for bit.
- * y has room for sum_b count[b] rows (at most B*N). x as in mpm_affinity.
+ *     singleton is copied bit for bit;
+ *   y_inv (optional, may be NULL): y_inv[y_off[b] + k] = 1 / max(||y_k||, 1e-12)
+ *     from the stored values of y in float32, summed in a fixed order (the same
+ *     on every run): the x_inv of y for the next insertion's affinity.
+ * src in the slot layout above (the workspace's src region after
+ * mpm_affinity_compact, or mpm_pair_compact's output); y has room for
+ * y_off[B] rows (at most B*N). x as in mpm_affinity.
  */
-int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count,
-                     int32_t B, int32_t N, int32_t D, int32_t dt,
-                     void* y, int32_t* y_off, void* stream);
+int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* y_off, int32_t B,
+                     int32_t N, int32_t D, int32_t dt, void* y, float* y_inv, void* stream);
 
 /*
- * mpm_pair_average that also writes y_inv[y_off[b] + k] = 1 / max(||y_k||, 1e-12)
- * for every merged row (device, float32, room for as many rows as y), from the
- * stored values of y in float32, summed in a fixed order (the same result on
- * every run). These are the x_inv that mpm_affinity_inv takes for y as the
- * next insertion's input. Errors as mpm_pair_average; a NULL or misaligned
- * y_inv returns MPM_ERR_INVALID_ARG.
- */
-int mpm_pair_average_inv(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count,
-                         int32_t B, int32_t N, int32_t D, int32_t dt, void* y, int32_t* y_off, float* y_inv,
-                         void* stream);
-
-/*
- * One MPM insertion (Alg. 1) = mpm_affinity, mpm_pair_compact_ws and
- * mpm_pair_average (src and count from the workspace) in order on `stream`.
- *   x, x_off: input tokens (dense or packed);
+ * One MPM insertion (Alg. 1) = mpm_affinity_compact, then mpm_pair_average
+ * (src from the workspace), in order on `stream`.
+ *   x, x_off, x_inv: input tokens (dense or packed) and optional given inverse
+ *       norms, as in mpm_affinity;
  *   y, y_off: merged tokens, packed (capacity B*N rows), offsets int32[B+1];
+ *   y_inv (may be NULL): inverse norms of the merged rows, as in mpm_pair_average;
  *   map: int32[B*N] merge map in slot layout (-1 beyond n_b);
- *   ws: workspace of at least mpm_workspace_bytes(B, N) bytes; nb, src and
- *       count are readable there after the call.
- * Feed (y, y_off) as (x, x_off) of the next insertion.
+ *   ws: workspace of at least mpm_workspace_bytes(B, N) bytes whose sync
+ *       region is zero (mpm_workspace_init); nb and src are readable there
+ *       after the call.
+ * Feed (y, y_off, y_inv) as (x, x_off, x_inv) of the next insertion.
  */
-int mpm_merge(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt,
-              void* y, int32_t* y_off, int32_t* map, void* ws, size_t ws_bytes, void* stream);
+int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D, int32_t dt,
+              int32_t schedule, void* y, int32_t* y_off, float* y_inv, int32_t* map, void* ws, size_t ws_bytes,
+              void* stream);
 
 /*
  * Composition of merge maps (Eq. 3): map_ab[b*N + i] = map_b[b*N + map_a[b*N + i]],

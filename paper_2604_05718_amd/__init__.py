@@ -3,10 +3,11 @@
 The computation lives in libmpm.so (hand-written HIP kernels behind the C ABI
 of include/mpm.h); this package is its thin torch binding.
 """
-from .api import (Merged, ScheduleResult, affinity_schedule_used, argmax, compose, compose_unmerge, merge,
-                  pair_average, pair_compact, run_schedule, set_affinity_schedule, unmerge, workspace_bytes)
+from .api import (Merged, Schedule, ScheduleResult, affinity, affinity_schedule_used, argmax, compose,
+                  compose_unmerge, insertion, merge, new_workspace, pair_average, pair_compact, run_schedule, unmerge,
+                  workspace_bytes)
 from ._lib import MPMError
 
-__all__ = ["Merged", "ScheduleResult", "MPMError", "affinity_schedule_used", "argmax", "compose", "compose_unmerge",
-           "merge", "pair_average", "pair_compact", "run_schedule", "set_affinity_schedule", "unmerge",
-           "workspace_bytes"]
+__all__ = ["Merged", "Schedule", "ScheduleResult", "MPMError", "affinity", "affinity_schedule_used", "argmax",
+           "compose", "compose_unmerge", "insertion", "merge", "new_workspace", "pair_average", "pair_compact",
+           "run_schedule", "unmerge", "workspace_bytes"]

@@ -38,17 +38,15 @@ SIGNATURES = {
     "mpm_last_hip_error": (ctypes.c_int, []),
     "mpm_workspace_bytes": (_sz, [_i32, _i32]),
     "mpm_workspace_offsets": (ctypes.c_int, [_i32, _i32, _szp, _szp, _szp, _szp, _szp]),
-    "mpm_affinity": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp]),
-    "mpm_affinity_timed": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp, _vp, _vp]),
-    "mpm_affinity_inv": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _sz, _vp, _vp, _vp]),
-    "mpm_set_affinity_schedule": (ctypes.c_int, [_i32]),
-    "mpm_affinity_schedule_used": (ctypes.c_int, [_i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_int32)]),
-    "mpm_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
+    "mpm_workspace_init": (ctypes.c_int, [_vp, _sz, _vp]),
+    "mpm_affinity": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _sz, _vp, _vp, _vp]),
+    "mpm_affinity_compact": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp, _vp,
+                                            _vp]),
+    "mpm_affinity_schedule_used": (ctypes.c_int, [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_int32)]),
+    "mpm_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "mpm_pair_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
-    "mpm_pair_compact_ws": (ctypes.c_int, [_vp, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp]),
     "mpm_pair_average": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp]),
-    "mpm_pair_average_inv": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
-    "mpm_merge": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "mpm_merge": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "mpm_compose": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp, _vp]),
     "mpm_compose_unmerge": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
     "mpm_unmerge": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
@@ -102,10 +100,10 @@ def load():
 
 
 def workspace_offsets(B: int, N: int) -> dict:
-    """Byte offsets of the workspace regions (nb, src, count, pv, pi)."""
+    """Byte offsets of the workspace regions (sync, nb, src, pv, pi)."""
     vals = [ctypes.c_size_t() for _ in range(5)]
     check("mpm_workspace_offsets", load().mpm_workspace_offsets(B, N, *[ctypes.byref(v) for v in vals]))
-    return dict(zip(("nb", "src", "count", "pv", "pi"), (v.value for v in vals)))
+    return dict(zip(("sync", "nb", "src", "pv", "pi"), (v.value for v in vals)))
 
 
 def check(fn: str, status: int) -> None:

@@ -61,53 +61,72 @@ def _rows(x: torch.Tensor, N: int | None, x_off: torch.Tensor | None):
     return x, x_off.numel() - 1, int(N), x.shape[1]
 
 
-def _workspace(B, N, device, ws=None):
-    need = workspace_bytes(B, N)
-    if ws is None or ws.numel() < need:
-        ws = torch.empty((need,), dtype=torch.uint8, device=device)
+def _sched(schedule: str) -> int:
+    try:
+        return SCHEDULES[schedule]
+    except KeyError:
+        raise ValueError(f"unknown schedule {schedule!r}; expected one of {sorted(SCHEDULES)}") from None
+
+
+def new_workspace(B: int, N: int, device) -> torch.Tensor:
+    """A workspace for B images of at most N tokens, its sync region zeroed (mpm_workspace_init)."""
+    ws = torch.empty((workspace_bytes(B, N),), dtype=torch.uint8, device=device)
+    _lib.check("mpm_workspace_init", _lib.load().mpm_workspace_init(_p(ws), ws.numel(), _stream()))
     return ws
 
 
-def argmax(x, x_off=None, N=None, with_best=False, ws=None):
+def _workspace(B, N, device, ws=None):
+    if ws is None or ws.numel() < workspace_bytes(B, N):
+        ws = new_workspace(B, N, device)
+    return ws
+
+
+def argmax(x, x_off=None, N=None, with_best=False, ws=None, schedule="auto"):
     """nb [B, N] int32 (and best [B, N] float32 cosines when ``with_best``)."""
     x2, B, N, D = _rows(x, N, x_off)
     nb = torch.empty((B, N), dtype=torch.int32, device=x.device)
     best = torch.empty((B, N), dtype=torch.float32, device=x.device) if with_best else None
     ws = _workspace(B, N, x.device, ws)
     lib = _lib.load()
-    _lib.check("mpm_argmax", lib.mpm_argmax(_p(x2), _p(x_off), B, N, D, _dt(x), _p(nb), _p(best), _p(ws),
-                                            ws.numel(), _stream()))
+    _lib.check("mpm_argmax", lib.mpm_argmax(_p(x2), _p(x_off), B, N, D, _dt(x), _sched(schedule), _p(nb), _p(best),
+                                            _p(ws), ws.numel(), _stream()))
     return (nb, best) if with_best else nb
 
 
+def affinity(x, x_off=None, N=None, x_inv=None, schedule="auto", ws=None, events=None):
+    """Runs mpm_affinity (the per-candidate-tile partials in the workspace); returns the
+    workspace. ``events``: optional (start, stop) timing events bound to its dispatches."""
+    x2, B, N, D = _rows(x, N, x_off)
+    ws = _workspace(B, N, x.device, ws)
+    ev0, ev1 = (None, None) if events is None else (c_event(e) for e in events)
+    _lib.check("mpm_affinity", _lib.load().mpm_affinity(_p(x2), _p(x_off), _p(x_inv), B, N, D, _dt(x),
+                                                        _sched(schedule), _p(ws), ws.numel(), ev0, ev1, _stream()))
+    return ws
+
+
 def pair_compact(nb, x_off=None):
-    """(map [B, N], src [B, N, 2], count [B]) from nb [B, N]."""
+    """(map [B, N], src [B, N, 2], y_off [B+1]) from nb [B, N]."""
     B, N = nb.shape
     dev = nb.device
     m = torch.empty((B, N), dtype=torch.int32, device=dev)
     src = torch.empty((B, N, 2), dtype=torch.int32, device=dev)
-    count = torch.empty((B,), dtype=torch.int32, device=dev)
+    y_off = torch.empty((B + 1,), dtype=torch.int32, device=dev)
     lib = _lib.load()
     _lib.check("mpm_pair_compact", lib.mpm_pair_compact(_p(nb.contiguous()), _p(x_off), B, N, _p(m), _p(src),
-                                                        _p(count), _stream()))
-    return m, src, count
+                                                        _p(y_off), _stream()))
+    return m, src, y_off
 
 
-def pair_average(x, src, count, x_off=None, N=None, with_inv=False):
-    """(y [B*N, D] packed at capacity, y_off [B+1]) cluster means; with ``with_inv``
-    also y_inv [B*N] float32, the inverse norms of the merged rows."""
+def pair_average(x, src, y_off, x_off=None, N=None, with_inv=False):
+    """y [B*N, D] packed at capacity: cluster means at the offsets y_off; with
+    ``with_inv`` also y_inv [B*N] float32, the inverse norms of the merged rows."""
     x2, B, N, D = _rows(x, N, x_off)
     y = torch.empty((B * N, D), dtype=x.dtype, device=x.device)
-    y_off = torch.empty((B + 1,), dtype=torch.int32, device=x.device)
+    y_inv = torch.empty((B * N,), dtype=torch.float32, device=x.device) if with_inv else None
     lib = _lib.load()
-    if not with_inv:
-        _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(x2), _p(x_off), _p(src), _p(count), B, N, D, _dt(x),
-                                                            _p(y), _p(y_off), _stream()))
-        return y, y_off
-    y_inv = torch.empty((B * N,), dtype=torch.float32, device=x.device)
-    _lib.check("mpm_pair_average_inv", lib.mpm_pair_average_inv(_p(x2), _p(x_off), _p(src), _p(count), B, N, D,
-                                                                _dt(x), _p(y), _p(y_off), _p(y_inv), _stream()))
-    return y, y_off, y_inv
+    _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(x2), _p(x_off), _p(src), _p(y_off), B, N, D, _dt(x),
+                                                        _p(y), _p(y_inv), _stream()))
+    return (y, y_inv) if with_inv else y
 
 
 def workspace_bytes(B: int, N: int) -> int:
@@ -118,24 +137,23 @@ SCHEDULES = {"auto": _lib.MPM_SCHEDULE_AUTO, "full": _lib.MPM_SCHEDULE_FULL, "sy
              "full_64": _lib.MPM_SCHEDULE_FULL_64}
 
 
-def set_affinity_schedule(mode: str) -> str:
-    """Select the affinity kernel's work schedule ("auto", "full", "symmetric" or
-    "full_64", process-wide); returns the previous one. Results do not depend on it."""
-    if mode not in SCHEDULES:
-        raise ValueError(f"unknown schedule {mode!r}; expected one of {sorted(SCHEDULES)}")
-    prev = _lib.load().mpm_set_affinity_schedule(SCHEDULES[mode])
-    if prev < 0:
-        raise _lib.MPMError("mpm_set_affinity_schedule", _lib.MPM_ERR_INVALID_ARG)
-    return {v: k for k, v in SCHEDULES.items()}[prev]
-
-
-def affinity_schedule_used(B: int, N: int, D: int, dtype: torch.dtype) -> str:
+def affinity_schedule_used(B: int, N: int, D: int, dtype: torch.dtype, schedule: str = "auto") -> str:
     """The schedule ("full", "symmetric" or "full_64") the affinity kernel runs for
-    this shape on the current device under the current mode."""
+    this shape and requested schedule on the current device."""
     out = ctypes.c_int32()
     _lib.check("mpm_affinity_schedule_used",
-               _lib.load().mpm_affinity_schedule_used(B, N, D, _DTYPES[dtype], ctypes.byref(out)))
+               _lib.load().mpm_affinity_schedule_used(B, N, D, _DTYPES[dtype], _sched(schedule), ctypes.byref(out)))
     return {v: k for k, v in SCHEDULES.items()}[out.value]
+
+
+def ws_view(ws: torch.Tensor, B: int, N: int, region: str) -> torch.Tensor:
+    """A workspace region as an int32 view: "nb" [B, N] or "src" [B, N, 2]."""
+    off = _lib.workspace_offsets(B, N)[region]
+    if region == "nb":
+        return ws[off:off + 4 * B * N].view(torch.int32).view(B, N)
+    if region == "src":
+        return ws[off:off + 8 * B * N].view(torch.int32).view(B, N, 2)
+    raise KeyError(region)
 
 
 @dataclass
@@ -143,41 +161,46 @@ class Merged:
     y: torch.Tensor       # [B*N, D] packed merged tokens (rows beyond y_off[B] unused)
     y_off: torch.Tensor   # [B+1] int32
     map: torch.Tensor     # [B, N] int32, -1 beyond n_b
-    ws: torch.Tensor      # workspace; nb lives at its start
+    ws: torch.Tensor      # workspace (nb and src regions readable)
     B: int
     N: int
     y_inv: torch.Tensor | None = None  # [B*N] float32 inverse norms of the rows of y, when asked for
 
     @property
     def nb(self) -> torch.Tensor:
-        return self.ws[: self.B * self.N * 4].view(torch.int32).view(self.B, self.N)
+        return ws_view(self.ws, self.B, self.N, "nb")
+
+    @property
+    def src(self) -> torch.Tensor:
+        return ws_view(self.ws, self.B, self.N, "src")
 
 
-def merge(x, x_off=None, N=None, ws=None) -> Merged:
-    """One MPM insertion (Alg. 1)."""
+def takes_norms(D: int, dtype: torch.dtype) -> bool:
+    """Whether the affinity accepts given inverse norms for rows of D values of this
+    dtype (bfloat16 rows a whole number of 64 bytes)."""
+    return dtype == torch.bfloat16 and (2 * D) % 64 == 0
+
+
+def merge(x, x_off=None, N=None, x_inv=None, want_inv=False, ws=None, schedule="auto") -> Merged:
+    """One MPM insertion (Alg. 1) through mpm_merge: the fused affinity + compaction,
+    then the pair average (also writing the inverse norms of the merged rows when
+    ``want_inv``). ``x_inv``: given inverse norms of the rows of x."""
     x2, B, N, D = _rows(x, N, x_off)
     dev = x.device
     ws = _workspace(B, N, dev, ws)
     y = torch.empty((B * N, D), dtype=x.dtype, device=dev)
     y_off = torch.empty((B + 1,), dtype=torch.int32, device=dev)
     m = torch.empty((B, N), dtype=torch.int32, device=dev)
+    y_inv = torch.empty((B * N,), dtype=torch.float32, device=dev) if want_inv else None
     lib = _lib.load()
-    _lib.check("mpm_merge", lib.mpm_merge(_p(x2), _p(x_off), B, N, D, _dt(x), _p(y), _p(y_off), _p(m), _p(ws),
-                                          ws.numel(), _stream()))
-    return Merged(y, y_off, m, ws, B, N)
+    _lib.check("mpm_merge", lib.mpm_merge(_p(x2), _p(x_off), _p(x_inv), B, N, D, _dt(x), _sched(schedule), _p(y),
+                                          _p(y_off), _p(y_inv), _p(m), _p(ws), ws.numel(), _stream()))
+    return Merged(y, y_off, m, ws, B, N, y_inv)
 
 
-def takes_norms(D: int, dtype: torch.dtype) -> bool:
-    """Whether mpm_affinity_inv accepts rows of D values of this dtype (bfloat16 rows
-    a whole number of 64 bytes)."""
-    return dtype == torch.bfloat16 and (2 * D) % 64 == 0
-
-
-def insertion(x, x_off=None, N=None, x_inv=None, want_inv=False, ws=None) -> Merged:
-    """One MPM insertion (Alg. 1) through the step entry points: affinity (with the
-    given inverse norms x_inv of the rows of x, if any), compaction from the
-    workspace partials, pair average (also writing the inverse norms of the merged
-    rows when want_inv). Equal to merge() when x_inv is None."""
+def insertion(x, x_off=None, N=None, x_inv=None, want_inv=False, ws=None, schedule="auto") -> Merged:
+    """One MPM insertion through the step entry points: mpm_affinity_compact, then
+    mpm_pair_average with the workspace's src. Equal to merge()."""
     x2, B, N, D = _rows(x, N, x_off)
     dev = x.device
     ws = _workspace(B, N, dev, ws)
@@ -186,20 +209,12 @@ def insertion(x, x_off=None, N=None, x_inv=None, want_inv=False, ws=None) -> Mer
     m = torch.empty((B, N), dtype=torch.int32, device=dev)
     y_inv = torch.empty((B * N,), dtype=torch.float32, device=dev) if want_inv else None
     lib, st, dt, n = _lib.load(), _stream(), _dt(x), ws.numel()
-    if x_inv is None:
-        _lib.check("mpm_affinity", lib.mpm_affinity(_p(x2), _p(x_off), B, N, D, dt, _p(ws), n, st))
-    else:
-        _lib.check("mpm_affinity_inv", lib.mpm_affinity_inv(_p(x2), _p(x_off), _p(x_inv), B, N, D, dt, _p(ws), n,
-                                                            None, None, st))
-    _lib.check("mpm_pair_compact_ws", lib.mpm_pair_compact_ws(_p(x_off), B, N, D, dt, _p(m), _p(ws), n, st))
-    off = _lib.workspace_offsets(B, N)
-    src, count = _p(ws[off["src"]:]), _p(ws[off["count"]:])
-    if y_inv is None:
-        _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(x2), _p(x_off), src, count, B, N, D, dt, _p(y),
-                                                            _p(y_off), st))
-    else:
-        _lib.check("mpm_pair_average_inv", lib.mpm_pair_average_inv(_p(x2), _p(x_off), src, count, B, N, D, dt,
-                                                                    _p(y), _p(y_off), _p(y_inv), st))
+    _lib.check("mpm_affinity_compact", lib.mpm_affinity_compact(_p(x2), _p(x_off), _p(x_inv), B, N, D, dt,
+                                                                _sched(schedule), _p(m), _p(y_off), _p(ws), n, None,
+                                                                None, st))
+    src = ws_view(ws, B, N, "src")
+    _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(x2), _p(x_off), _p(src), _p(y_off), B, N, D, dt, _p(y),
+                                                        _p(y_inv), st))
     return Merged(y, y_off, m, ws, B, N, y_inv)
 
 
@@ -253,7 +268,7 @@ class ScheduleResult:
     out: torch.Tensor     # reconstructed grid [B, N, D]
 
 
-def run_schedule(x, insertions: int = 2, workspaces=None) -> ScheduleResult:
+def run_schedule(x, insertions: int = 2, workspaces=None, schedule: str = "auto") -> ScheduleResult:
     """Insertions with identity blocks in between (Sec. 3.3), composed maps
     (Eq. 3) and one gather back to the full grid (Eq. 4). Each insertion after the
     first takes the inverse norms of its input rows from the pair average that
@@ -265,7 +280,7 @@ def run_schedule(x, insertions: int = 2, workspaces=None) -> ScheduleResult:
     rstar = None
     for s in range(insertions):
         ws = None if workspaces is None else workspaces[s]
-        m = insertion(cur, cur_off, N=N, x_inv=cur_inv, want_inv=norms and s + 1 < insertions, ws=ws)
+        m = merge(cur, cur_off, N=N, x_inv=cur_inv, want_inv=norms and s + 1 < insertions, ws=ws, schedule=schedule)
         stages.append(m)
         rstar = m.map if rstar is None else compose(rstar, m.map)
         cur, cur_off, cur_inv = m.y, m.y_off, m.y_inv
@@ -278,31 +293,31 @@ class Schedule:
     allocated once, so ``run`` only launches kernels (no allocation, no host
     synchronisation). Stage s consumes stage s-1's packed output (Sec. 3.3);
     the composed map and the reconstruction follow (Eq. 3, Eq. 4). Each
-    insertion runs the three kernels of ``mpm_merge`` through its step entry
-    points (affinity, compaction, average), so they can be timed one by one.
+    insertion runs mpm_merge's two steps through their entry points (the fused
+    affinity + compaction, then the pair average), so they can be timed one by
+    one; the last composition runs inside the gather.
 
     ``run(x, marks=None, affinity_events=None)``: when ``marks`` is a list of
     ``n_marks()`` torch.cuda.Event objects, event k is recorded on the current
-    stream just before kernel k (in ``kernel_names`` order) and the last one
-    after the gather, so consecutive events bracket single kernels. When
+    stream just before kernel step k (in ``kernel_names`` order) and the last one
+    after the gather, so consecutive events bracket single steps. When
     ``affinity_events`` is a list of one (start, stop) pair of timing events
-    per insertion, each pair is bound to that insertion's affinity kernel
-    itself (``mpm_affinity_timed``): no stream command is added, and
-    ``start.elapsed_time(stop)`` is the kernel's duration. The events must have
-    been recorded once before (torch creates them lazily)."""
+    per insertion, each pair is bound to that insertion's affinity launches
+    themselves: no stream command is added, and ``start.elapsed_time(stop)`` is
+    their duration. The events must have been recorded once before (torch
+    creates them lazily)."""
 
-    def __init__(self, B: int, N: int, D: int, dtype: torch.dtype, insertions: int = 2, device="cuda"):
+    def __init__(self, B: int, N: int, D: int, dtype: torch.dtype, insertions: int = 2, device="cuda",
+                 schedule: str = "auto"):
         if insertions < 1:
             raise ValueError("at least one insertion")
         self.B, self.N, self.D, self.dtype, self.insertions = B, N, D, dtype, insertions
+        self.schedule = _sched(schedule)
         dev = torch.device(device)
         i32 = dict(dtype=torch.int32, device=dev)
-        nbytes = workspace_bytes(B, N)
-        off = _lib.workspace_offsets(B, N)
-        self.ws = [torch.empty((nbytes,), dtype=torch.uint8, device=dev) for _ in range(insertions)]
-        self.nb = [w[off["nb"]:off["nb"] + 4 * B * N].view(torch.int32).view(B, N) for w in self.ws]
-        self.src = [w[off["src"]:off["src"] + 8 * B * N].view(torch.int32).view(B, N, 2) for w in self.ws]
-        self.count = [w[off["count"]:off["count"] + 4 * B].view(torch.int32) for w in self.ws]
+        self.ws = [new_workspace(B, N, dev) for _ in range(insertions)]
+        self.nb = [ws_view(w, B, N, "nb") for w in self.ws]
+        self.src = [ws_view(w, B, N, "src") for w in self.ws]
         self.map = [torch.empty((B, N), **i32) for _ in range(insertions)]
         self.y = [torch.empty((B * N, D), dtype=dtype, device=dev) for _ in range(insertions)]
         self.y_off = [torch.empty((B + 1,), **i32) for _ in range(insertions)]
@@ -321,7 +336,7 @@ class Schedule:
     def kernel_names(self) -> list:
         names = []
         for s in range(self.insertions):
-            names += [f"affinity{s + 1}", f"compact{s + 1}", f"average{s + 1}"]
+            names += [f"affinity+compact{s + 1}", f"average{s + 1}"]
         if self.insertions == 1:
             return names + ["unmerge"]
         # the last composition runs inside the gather (mpm_compose_unmerge)
@@ -347,26 +362,13 @@ class Schedule:
             ws = self.ws[s]
             mark()
             ev0, ev1 = (None, None) if affinity_events is None else (c_event(e) for e in affinity_events[s])
-            if cur_inv is not None:
-                _lib.check("mpm_affinity_inv", lib.mpm_affinity_inv(_p(cur), _p(cur_off), _p(cur_inv), B, N, D, dt,
-                                                                    _p(ws), ws.numel(), ev0, ev1, st))
-            elif affinity_events is None:
-                _lib.check("mpm_affinity", lib.mpm_affinity(_p(cur), _p(cur_off), B, N, D, dt, _p(ws), ws.numel(), st))
-            else:
-                _lib.check("mpm_affinity_timed", lib.mpm_affinity_timed(_p(cur), _p(cur_off), B, N, D, dt, _p(ws),
-                                                                        ws.numel(), ev0, ev1, st))
+            _lib.check("mpm_affinity_compact", lib.mpm_affinity_compact(
+                _p(cur), _p(cur_off), _p(cur_inv), B, N, D, dt, self.schedule, _p(self.map[s]), _p(self.y_off[s]),
+                _p(ws), ws.numel(), ev0, ev1, st))
             mark()
-            _lib.check("mpm_pair_compact_ws", lib.mpm_pair_compact_ws(_p(cur_off), B, N, D, dt, _p(self.map[s]),
-                                                                      _p(ws), ws.numel(), st))
-            mark()
-            if self.y_inv[s] is None:
-                _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(cur), _p(cur_off), _p(self.src[s]),
-                                                                    _p(self.count[s]), B, N, D, dt, _p(self.y[s]),
-                                                                    _p(self.y_off[s]), st))
-            else:
-                _lib.check("mpm_pair_average_inv", lib.mpm_pair_average_inv(
-                    _p(cur), _p(cur_off), _p(self.src[s]), _p(self.count[s]), B, N, D, dt, _p(self.y[s]),
-                    _p(self.y_off[s]), _p(self.y_inv[s]), st))
+            _lib.check("mpm_pair_average", lib.mpm_pair_average(_p(cur), _p(cur_off), _p(self.src[s]),
+                                                                _p(self.y_off[s]), B, N, D, dt, _p(self.y[s]),
+                                                                _p(self.y_inv[s]), st))
             cur, cur_off, cur_inv = self.y[s], self.y_off[s], self.y_inv[s]
         if self.insertions == 1:
             mark()

@@ -25,8 +25,6 @@
 // tile and no separate normalisation pass exists.
 #include <hip/hip_ext.h>
 
-#include <atomic>
-
 #include "mpm_device.h"
 #include "mpm_launch.h"
 
@@ -1017,8 +1015,6 @@ static_assert(kTWQ * kTNT * 32 == kTCT && kPCT % kTCT == 0, "square small blocks
 static_assert(kSWC * kSMT * 32 == kPCT && kSWQ * kSNT * 32 == kPCT && kPWQ * kPNT * 32 == kPCT,
               "both schedules use 256 x 256 tiles, so their partials share one layout");
 
-std::atomic<int> g_schedule{kScheduleAuto};
-
 bool use_persistent(int D, int dt) { return ((long)D * (dt == kBf16 ? 2 : 4)) % kPCB == 0; }
 
 }  // namespace
@@ -1087,32 +1083,26 @@ hipError_t launch_staged(const void* x, const int32_t* x_off, int B, int N, int 
 // Partial slots reserved per token: enough for the smallest block width any schedule uses.
 int partial_tiles(int N) { return (N + kTCT - 1) / kTCT; }
 
-// Whether a persistent launch of this shape uses the 64 x 64 blocks (no device query).
-bool small_blocks(int B, int N)
+bool valid_schedule(int schedule)
 {
-    const int mode = g_schedule.load();
-    if (mode != kScheduleAuto) return mode == kScheduleFull64;
+    return schedule == kScheduleAuto || schedule == kScheduleFull || schedule == kScheduleSymmetric ||
+           schedule == kScheduleFull64;
+}
+
+namespace {
+
+// Whether a persistent launch of this shape and requested schedule uses the 64 x 64
+// blocks (no device query).
+bool small_blocks(int B, int N, int schedule)
+{
+    if (schedule != kScheduleAuto) return schedule == kScheduleFull64;
     const long nqb = (N + kPCT - 1) / kPCT;
     return (long)B * nqb * nqb <= kSmallItems;
 }
 
-int partial_tile_width(int B, int D, int dt, int N)
+bool symmetric_schedule(int B, int N, int xcds, int slots, int schedule)
 {
-    if (!use_persistent(D, dt)) return N;
-    return small_blocks(B, N) ? kTCT : kPCT;
-}
-
-int set_affinity_schedule(int mode)
-{
-    if (mode != kScheduleAuto && mode != kScheduleFull && mode != kScheduleSymmetric && mode != kScheduleFull64)
-        return -1;
-    return g_schedule.exchange(mode);
-}
-
-bool symmetric_schedule(int B, int N, int xcds, int slots)
-{
-    const int mode = g_schedule.load();
-    if (mode != kScheduleAuto) return mode == kScheduleSymmetric;
+    if (schedule != kScheduleAuto) return schedule == kScheduleSymmetric;
     // Rounds of work items per workgroup slot under either schedule. An off-diagonal
     // item of the symmetric one costs about a fifth more (its reverse direction), so
     // it pays only when it saves more than that in rounds.
@@ -1123,23 +1113,31 @@ bool symmetric_schedule(int B, int N, int xcds, int slots)
     return 5 * sym < 4 * full;
 }
 
-hipError_t affinity_schedule(int B, int N, int D, int dt, int* schedule)
+}  // namespace
+
+int partial_tile_width(int B, int D, int dt, int N, int schedule)
 {
-    *schedule = kScheduleFull;
+    if (!use_persistent(D, dt)) return N;
+    return small_blocks(B, N, schedule) ? kTCT : kPCT;
+}
+
+hipError_t affinity_schedule(int B, int N, int D, int dt, int schedule, int* used)
+{
+    *used = kScheduleFull;
     if (!use_persistent(D, dt)) return hipSuccess;  // the staged kernel covers every pair
-    if (small_blocks(B, N)) {
-        *schedule = kScheduleFull64;
+    if (small_blocks(B, N, schedule)) {
+        *used = kScheduleFull64;
         return hipSuccess;
     }
     const int cus = device_cus();
     if (cus <= 0) return hipErrorInvalidDevice;
     const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
-    if (symmetric_schedule(B, N, xcds, cus * kPWGS / xcds)) *schedule = kScheduleSymmetric;
+    if (symmetric_schedule(B, N, xcds, cus * kPWGS / xcds, schedule)) *used = kScheduleSymmetric;
     return hipSuccess;
 }
 
-hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, int D, int dt, float* pv, int32_t* pi,
-                           hipStream_t stream, hipEvent_t start, hipEvent_t stop, const float* xinv)
+hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, int D, int dt, int schedule, float* pv,
+                           int32_t* pi, hipStream_t stream, hipEvent_t start, hipEvent_t stop, const float* xinv)
 {
     const int T = partial_tiles(N);
     if (xinv && !affinity_takes_norms(D, dt)) return hipErrorInvalidValue;  // those kernels sum their own norms
@@ -1150,7 +1148,7 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
         // workgroups by XCD.
         const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
         const int groups = cus * kPWGS;
-        if (small_blocks(B, N)) {
+        if (small_blocks(B, N, schedule)) {
             if (dt == kBf16)
                 launch_persistent<Bf16, kTWC, kTWQ, kTMT, kTNT, false>(x, x_off, xinv, B, N, D, T, xcds, groups, pv, pi,
                                                                         stream, start, stop);
@@ -1159,7 +1157,7 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
                                                                        stream, start, stop);
             return hipGetLastError();
         }
-        const bool sym = symmetric_schedule(B, N, xcds, groups / xcds);
+        const bool sym = symmetric_schedule(B, N, xcds, groups / xcds, schedule);
         if (dt == kBf16) {
             if (sym)
                 launch_persistent<Bf16, kSWC, kSWQ, kSMT, kSNT, true>(x, x_off, xinv, B, N, D, T, xcds, groups, pv, pi,

@@ -4,6 +4,7 @@
 
 #include <stdint.h>
 
+
 #include "../../include/mpm.h"
 #include "mpm_launch.h"
 
@@ -45,16 +46,20 @@ bool ok_opt_int_ptr(const void* p) { return p == nullptr || aligned(p, 4); }
 constexpr size_t kAlign = 256;
 size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
+// The sync region: one arrival counter per image plus the images-done counter, at
+// the start of every workspace and of the same size for every shape.
+constexpr size_t kSyncWords = (size_t)MPM_MAX_B + 1;
+
 struct Workspace {
+    int32_t* sync;
     int32_t* nb;
     int32_t* src;
-    int32_t* count;
     float* pv;
     int32_t* pi;
 };
 
 struct Offsets {
-    size_t nb, src, count, pv, pi, total;
+    size_t sync, nb, src, pv, pi, total;
 };
 
 Offsets workspace_offsets(int32_t B, int32_t N)
@@ -62,10 +67,10 @@ Offsets workspace_offsets(int32_t B, int32_t N)
     const size_t slots = (size_t)B * (size_t)N;
     const size_t partial = slots * (size_t)mpm::partial_tiles(N);
     Offsets o;
-    o.nb = 0;
+    o.sync = 0;
+    o.nb = o.sync + round_up(kSyncWords * sizeof(int32_t));
     o.src = o.nb + round_up(slots * sizeof(int32_t));
-    o.count = o.src + round_up(2 * slots * sizeof(int32_t));
-    o.pv = o.count + round_up((size_t)B * sizeof(int32_t));
+    o.pv = o.src + round_up(2 * slots * sizeof(int32_t));
     o.pi = o.pv + round_up(partial * sizeof(float));
     o.total = o.pi + round_up(partial * sizeof(int32_t));
     return o;
@@ -78,9 +83,9 @@ int carve(void* ws, size_t ws_bytes, int32_t B, int32_t N, Workspace* w)
     const Offsets o = workspace_offsets(B, N);
     if (ws_bytes < o.total) return MPM_ERR_WORKSPACE;
     char* p = static_cast<char*>(ws);
+    w->sync = reinterpret_cast<int32_t*>(p + o.sync);
     w->nb = reinterpret_cast<int32_t*>(p + o.nb);
     w->src = reinterpret_cast<int32_t*>(p + o.src);
-    w->count = reinterpret_cast<int32_t*>(p + o.count);
     w->pv = reinterpret_cast<float*>(p + o.pv);
     w->pi = reinterpret_cast<int32_t*>(p + o.pi);
     return MPM_OK;
@@ -88,7 +93,19 @@ int carve(void* ws, size_t ws_bytes, int32_t B, int32_t N, Workspace* w)
 
 hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
-// nb from the affinity partials, then mutual pairs and compact ids. With few
+// Shared checks of the affinity entry points.
+int check_affinity(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D,
+                   int32_t dt, int32_t schedule)
+{
+    const int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!mpm::valid_schedule(schedule)) return MPM_ERR_INVALID_ARG;
+    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_opt_int_ptr(x_inv)) return MPM_ERR_INVALID_ARG;
+    if (x_inv && !mpm::affinity_takes_norms(D, dt)) return MPM_ERR_UNSUPPORTED;
+    return MPM_OK;
+}
+
+// nb from the affinity partials, then mutual pairs, compact ids and offsets. With few
 // candidate tiles the compaction kernel (one workgroup per image) reduces the
 // partials itself; with more, that serial reduction dominates, so a fully
 // parallel reduction writes nb first and the compaction reads it. A batch of a
@@ -99,15 +116,25 @@ constexpr int kFusedReduceMaxTilesFewImages = 16;
 constexpr int kFewImages = 8;
 
 hipError_t compact_from_partials(const Workspace& w, const int32_t* x_off, int32_t B, int32_t N, int32_t D,
-                                 int32_t dt, int32_t* map, hipStream_t st)
+                                 int32_t dt, int32_t schedule, int32_t* map, int32_t* y_off, hipStream_t st)
 {
     const int T = mpm::partial_tiles(N);
-    const int ct = mpm::partial_tile_width(B, D, dt, N);
+    const int ct = mpm::partial_tile_width(B, D, dt, N, schedule);
     const int fused_max = B <= kFewImages ? kFusedReduceMaxTilesFewImages : kFusedReduceMaxTiles;
     if ((N + ct - 1) / ct <= fused_max)
-        return mpm::launch_pair_compact_partials(w.pv, w.pi, T, ct, w.nb, x_off, B, N, map, w.src, w.count, st);
-    hipError_t e = mpm::launch_reduce_partials(w.pv, w.pi, nullptr, x_off, B, N, D, dt, w.nb, nullptr, st);
-    if (e == hipSuccess) e = mpm::launch_pair_compact(w.nb, x_off, B, N, map, w.src, w.count, st);
+        return mpm::launch_pair_compact_partials(w.pv, w.pi, T, ct, w.nb, x_off, B, N, map, w.src, y_off, w.sync, st);
+    hipError_t e = mpm::launch_reduce_partials(w.pv, w.pi, ct, nullptr, x_off, B, N, D, dt, w.nb, nullptr, st);
+    if (e == hipSuccess) e = mpm::launch_pair_compact(w.nb, x_off, B, N, map, w.src, y_off, w.sync, st);
+    return e;
+}
+
+// One insertion's affinity (events bound to its launches) and compaction into the carved workspace.
+hipError_t affinity_compact(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N,
+                            int32_t D, int32_t dt, int32_t schedule, int32_t* map, int32_t* y_off,
+                            const Workspace& w, hipEvent_t start, hipEvent_t stop, hipStream_t st)
+{
+    hipError_t e = mpm::launch_affinity(x, x_off, B, N, D, dt, schedule, w.pv, w.pi, st, start, stop, x_inv);
+    if (e == hipSuccess) e = compact_from_partials(w, x_off, B, N, D, dt, schedule, map, y_off, st);
     return e;
 }
 
@@ -115,7 +142,7 @@ hipError_t compact_from_partials(const Workspace& w, const int32_t* x_off, int32
 
 extern "C" {
 
-const char* mpm_version(void) { return "mpm 0.1.0 gfx950"; }
+const char* mpm_version(void) { return "mpm 0.2.0 gfx950"; }
 
 const char* mpm_status_string(int status)
 {
@@ -137,141 +164,112 @@ size_t mpm_workspace_bytes(int32_t B, int32_t N)
     return workspace_offsets(B, N).total;
 }
 
-int mpm_workspace_offsets(int32_t B, int32_t N, size_t* nb, size_t* src, size_t* count, size_t* pv, size_t* pi)
+int mpm_workspace_offsets(int32_t B, int32_t N, size_t* sync, size_t* nb, size_t* src, size_t* pv, size_t* pi)
 {
     if (B < 1 || N < 1) return MPM_ERR_INVALID_ARG;
     const Offsets o = workspace_offsets(B, N);
+    if (sync) *sync = o.sync;
     if (nb) *nb = o.nb;
     if (src) *src = o.src;
-    if (count) *count = o.count;
     if (pv) *pv = o.pv;
     if (pi) *pi = o.pi;
     return MPM_OK;
 }
 
-int mpm_affinity(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* ws,
-                 size_t ws_bytes, void* stream)
+int mpm_workspace_init(void* ws, size_t ws_bytes, void* stream)
 {
-    int s = check_rows(B, N, D, dt);
-    if (s != MPM_OK) return s;
-    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off)) return MPM_ERR_INVALID_ARG;
-    Workspace w;
-    if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
-    return hip_status(mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, as_stream(stream)));
+    if (ws == nullptr || !aligned(ws, kAlign)) return MPM_ERR_INVALID_ARG;
+    if (ws_bytes < kSyncWords * sizeof(int32_t)) return MPM_ERR_WORKSPACE;
+    return hip_status(mpm::launch_zero_words(static_cast<int32_t*>(ws), (long)kSyncWords, as_stream(stream)));
 }
 
-int mpm_affinity_timed(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* ws,
-                       size_t ws_bytes, void* start_event, void* stop_event, void* stream)
+int mpm_affinity(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D, int32_t dt,
+                 int32_t schedule, void* ws, size_t ws_bytes, void* start_event, void* stop_event, void* stream)
 {
-    int s = check_rows(B, N, D, dt);
+    int s = check_affinity(x, x_off, x_inv, B, N, D, dt, schedule);
     if (s != MPM_OK) return s;
-    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off)) return MPM_ERR_INVALID_ARG;
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
-    return hip_status(mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, as_stream(stream),
-                                           static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event)));
-}
-
-int mpm_affinity_inv(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D,
-                     int32_t dt, void* ws, size_t ws_bytes, void* start_event, void* stop_event, void* stream)
-{
-    int s = check_rows(B, N, D, dt);
-    if (s != MPM_OK) return s;
-    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(x_inv)) return MPM_ERR_INVALID_ARG;
-    if (!mpm::affinity_takes_norms(D, dt)) return MPM_ERR_UNSUPPORTED;
-    Workspace w;
-    if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
-    return hip_status(mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, as_stream(stream),
+    return hip_status(mpm::launch_affinity(x, x_off, B, N, D, dt, schedule, w.pv, w.pi, as_stream(stream),
                                            static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event),
                                            x_inv));
 }
 
-int mpm_set_affinity_schedule(int32_t mode) { return mpm::set_affinity_schedule(mode); }
+int mpm_affinity_compact(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D,
+                         int32_t dt, int32_t schedule, int32_t* map, int32_t* y_off, void* ws, size_t ws_bytes,
+                         void* start_event, void* stop_event, void* stream)
+{
+    int s = check_affinity(x, x_off, x_inv, B, N, D, dt, schedule);
+    if (s != MPM_OK) return s;
+    if (!ok_int_ptr(map) || !ok_int_ptr(y_off)) return MPM_ERR_INVALID_ARG;
+    Workspace w;
+    if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
+    return hip_status(affinity_compact(x, x_off, x_inv, B, N, D, dt, schedule, map, y_off, w,
+                                       static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event),
+                                       as_stream(stream)));
+}
 
-int mpm_affinity_schedule_used(int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* schedule)
+int mpm_affinity_schedule_used(int32_t B, int32_t N, int32_t D, int32_t dt, int32_t schedule, int32_t* used)
 {
     const int s = check_rows(B, N, D, dt);
     if (s != MPM_OK) return s;
-    if (!schedule) return MPM_ERR_INVALID_ARG;
+    if (!used || !mpm::valid_schedule(schedule)) return MPM_ERR_INVALID_ARG;
     int sc = 0;
-    const int st = hip_status(mpm::affinity_schedule(B, N, D, dt, &sc));
-    if (st == MPM_OK) *schedule = sc;
+    const int st = hip_status(mpm::affinity_schedule(B, N, D, dt, schedule, &sc));
+    if (st == MPM_OK) *used = sc;
     return st;
 }
 
-int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* nb,
-               float* best, void* ws, size_t ws_bytes, void* stream)
+int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t schedule,
+               int32_t* nb, float* best, void* ws, size_t ws_bytes, void* stream)
 {
-    int s = check_rows(B, N, D, dt);
+    int s = check_affinity(x, x_off, nullptr, B, N, D, dt, schedule);
     if (s != MPM_OK) return s;
-    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(nb) || !ok_opt_int_ptr(best))
-        return MPM_ERR_INVALID_ARG;
+    if (!ok_int_ptr(nb) || !ok_opt_int_ptr(best)) return MPM_ERR_INVALID_ARG;
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     const hipStream_t st = as_stream(stream);
-    hipError_t e = mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, st);
-    if (e == hipSuccess) e = mpm::launch_reduce_partials(w.pv, w.pi, x, x_off, B, N, D, dt, nb, best, st);
+    hipError_t e = mpm::launch_affinity(x, x_off, B, N, D, dt, schedule, w.pv, w.pi, st, nullptr, nullptr, nullptr);
+    if (e == hipSuccess)
+        e = mpm::launch_reduce_partials(w.pv, w.pi, mpm::partial_tile_width(B, D, dt, N, schedule), x, x_off, B, N, D,
+                                        dt, nb, best, st);
     return hip_status(e);
 }
 
 int mpm_pair_compact(const int32_t* nb, const int32_t* x_off, int32_t B, int32_t N, int32_t* map, int32_t* src,
-                     int32_t* count, void* stream)
+                     int32_t* y_off, void* stream)
 {
     const int s = check_shape(B, N);
     if (s != MPM_OK) return s;
-    if (!ok_int_ptr(nb) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(map) || !ok_int_ptr(src) || !ok_int_ptr(count))
+    if (!ok_int_ptr(nb) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(map) || !ok_int_ptr(src) || !ok_int_ptr(y_off))
         return MPM_ERR_INVALID_ARG;
-    return hip_status(mpm::launch_pair_compact(nb, x_off, B, N, map, src, count, as_stream(stream)));
+    return hip_status(mpm::launch_pair_compact(nb, x_off, B, N, map, src, y_off, nullptr, as_stream(stream)));
 }
 
-int mpm_pair_compact_ws(const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t* map, void* ws,
-                        size_t ws_bytes, void* stream)
-{
-    int s = check_rows(B, N, D, dt);
-    if (s != MPM_OK) return s;
-    if (!ok_opt_int_ptr(x_off) || !ok_int_ptr(map)) return MPM_ERR_INVALID_ARG;
-    Workspace w;
-    if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
-    return hip_status(compact_from_partials(w, x_off, B, N, D, dt, map, as_stream(stream)));
-}
-
-int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count, int32_t B,
-                     int32_t N, int32_t D, int32_t dt, void* y, int32_t* y_off, void* stream)
+int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* y_off, int32_t B,
+                     int32_t N, int32_t D, int32_t dt, void* y, float* y_inv, void* stream)
 {
     const int s = check_rows(B, N, D, dt);
     if (s != MPM_OK) return s;
-    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(src) || !ok_int_ptr(count) || !ok_rows_ptr(y) ||
-        !ok_int_ptr(y_off))
+    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(src) || !ok_int_ptr(y_off) || !ok_rows_ptr(y) ||
+        !ok_opt_int_ptr(y_inv))
         return MPM_ERR_INVALID_ARG;
-    return hip_status(mpm::launch_pair_average(x, x_off, src, count, B, N, D, dt, y, y_off, as_stream(stream)));
+    return hip_status(mpm::launch_pair_average(x, x_off, src, y_off, B, N, D, dt, y, y_inv, as_stream(stream)));
 }
 
-int mpm_pair_average_inv(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count, int32_t B,
-                         int32_t N, int32_t D, int32_t dt, void* y, int32_t* y_off, float* y_inv, void* stream)
+int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D, int32_t dt,
+              int32_t schedule, void* y, int32_t* y_off, float* y_inv, int32_t* map, void* ws, size_t ws_bytes,
+              void* stream)
 {
-    const int s = check_rows(B, N, D, dt);
+    int s = check_affinity(x, x_off, x_inv, B, N, D, dt, schedule);
     if (s != MPM_OK) return s;
-    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(src) || !ok_int_ptr(count) || !ok_rows_ptr(y) ||
-        !ok_int_ptr(y_off) || !ok_int_ptr(y_inv))
-        return MPM_ERR_INVALID_ARG;
-    return hip_status(
-        mpm::launch_pair_average(x, x_off, src, count, B, N, D, dt, y, y_off, as_stream(stream), y_inv));
-}
-
-int mpm_merge(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, void* y,
-              int32_t* y_off, int32_t* map, void* ws, size_t ws_bytes, void* stream)
-{
-    int s = check_rows(B, N, D, dt);
-    if (s != MPM_OK) return s;
-    if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_rows_ptr(y) || !ok_int_ptr(y_off) || !ok_int_ptr(map))
+    if (!ok_rows_ptr(y) || !ok_int_ptr(y_off) || !ok_opt_int_ptr(y_inv) || !ok_int_ptr(map))
         return MPM_ERR_INVALID_ARG;
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     const hipStream_t st = as_stream(stream);
-    hipError_t e = mpm::launch_affinity(x, x_off, B, N, D, dt, w.pv, w.pi, st);
-    if (e == hipSuccess)
-        e = compact_from_partials(w, x_off, B, N, D, dt, map, st);
-    if (e == hipSuccess) e = mpm::launch_pair_average(x, x_off, w.src, w.count, B, N, D, dt, y, y_off, st);
+    hipError_t e = affinity_compact(x, x_off, x_inv, B, N, D, dt, schedule, map, y_off, w, nullptr, nullptr, st);
+    if (e == hipSuccess) e = mpm::launch_pair_average(x, x_off, w.src, y_off, B, N, D, dt, y, y_inv, st);
     return hip_status(e);
 }
 

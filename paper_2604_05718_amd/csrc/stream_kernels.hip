@@ -74,19 +74,22 @@ __device__ __forceinline__ void for_each_vec_batched(long f0, long f1, int vpr, 
     }
 }
 
-// Sum of count[0..b) by the first wave; broadcast through LDS.
-__device__ __forceinline__ int image_offset(const int32_t* count, int b)
+// Output rows of image b in a packed buffer of capacity B*N rows, from offsets that
+// the compaction wrote. The clamps change nothing for offsets that follow the
+// contract (0 <= count <= N, monotone, within capacity); they keep a kernel in
+// bounds if an upstream fault ever left them unwritten.
+struct Span {
+    int off, cnt;
+};
+__device__ __forceinline__ Span output_span(const int32_t* y_off, int b, int N, int B)
 {
-    __shared__ int off_sh;
-    if (threadIdx.x < kWave) {
-        int s = 0;
-        for (int k = threadIdx.x; k < b; k += kWave) s += count[k];
-        s = wave_sum(s);
-        if (threadIdx.x == 0) off_sh = s;
-    }
-    __syncthreads();
-    return off_sh;
+    const int o = y_off[b];
+    const int c = min(max(y_off[b + 1] - o, 0), N);
+    const long cap = (long)B * N;
+    return Span{(int)min(max((long)o, 0L), cap - c), c};
 }
+// A source row index from src, kept inside the image's n rows (same contract note).
+__device__ __forceinline__ int clamp_row(int r, int n) { return min(max(r, 0), n - 1); }
 
 // Sum of squares of the values of one 16-byte vector, in float32.
 __device__ __forceinline__ float vec_sumsq(u32x4 v, Bf16)
@@ -110,28 +113,23 @@ __device__ __forceinline__ float vec_sumsq(u32x4 v, F32)
 template <class S>
 __global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, const int32_t* __restrict__ src,
-    const int32_t* __restrict__ count, int N, int D, int rows_per_block, uint8_t* __restrict__ y,
-    int32_t* __restrict__ y_off)
+    const int32_t* __restrict__ y_off, int N, int D, int rows_per_block, uint8_t* __restrict__ y)
 {
     const int b = blockIdx.y;
-    const int off = image_offset(count, b);
-    const int cnt = count[b];
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        y_off[b + 1] = off + cnt;
-        if (b == 0) y_off[0] = 0;
-    }
+    const Span sp = output_span(y_off, b, N, gridDim.y);
     const int k0 = blockIdx.x * rows_per_block;
-    const int k1 = min(cnt, k0 + rows_per_block);
+    const int k1 = min(sp.cnt, k0 + rows_per_block);
     if (k0 >= k1) return;
     const long rowbytes = (long)D * S::kBytes;
     const int vpr = (int)(rowbytes / 16);
+    const int nx = x_off ? x_off[b + 1] - x_off[b] : N;
     const uint8_t* ximg = x + (long)(x_off ? x_off[b] : b * N) * rowbytes;
-    uint8_t* yimg = y + (long)off * rowbytes;
+    uint8_t* yimg = y + (long)sp.off * rowbytes;
     const int32_t* srcb = src + 2L * b * N;
     for_each_vec_batched<kAverageBatch>((long)k0 * vpr, (long)k1 * vpr, vpr,
         [&](long k, int c) {
-            const int ia = srcb[2 * k];
-            const int ib = srcb[2 * k + 1];
+            const int ia = clamp_row(srcb[2 * k], nx);
+            const int ib = clamp_row(srcb[2 * k + 1], nx);
             const u32x4 va = load16(ximg + ia * rowbytes + c * 16);
             u32x4 out = va;  // a singleton is copied bit for bit
             if (ib != ia) out = mean16(va, load16(ximg + ib * rowbytes + c * 16), S{});
@@ -149,16 +147,11 @@ __global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
 template <class S>
 __global__ __launch_bounds__(kRowThreads) void pair_average_inv_kernel(
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, const int32_t* __restrict__ src,
-    const int32_t* __restrict__ count, int N, int D, uint8_t* __restrict__ y, int32_t* __restrict__ y_off,
-    float* __restrict__ y_inv)
+    const int32_t* __restrict__ y_off, int N, int D, uint8_t* __restrict__ y, float* __restrict__ y_inv)
 {
     const int b = blockIdx.y;
-    const int off = image_offset(count, b);
-    const int cnt = count[b];
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        y_off[b + 1] = off + cnt;
-        if (b == 0) y_off[0] = 0;
-    }
+    const Span sp = output_span(y_off, b, N, gridDim.y);
+    const int off = sp.off, cnt = sp.cnt;
     const long rowbytes = (long)D * S::kBytes;
     const int vpr = (int)(rowbytes / 16);
     const int G = inv_lanes(vpr);
@@ -167,11 +160,12 @@ __global__ __launch_bounds__(kRowThreads) void pair_average_inv_kernel(
     const int k = k0 + (int)threadIdx.x / G;  // this group's row
     const int j = threadIdx.x % G;
     const bool live = k < cnt;
+    const int nx = x_off ? x_off[b + 1] - x_off[b] : N;
     const uint8_t* ximg = x + (long)(x_off ? x_off[b] : b * N) * rowbytes;
     int ia = 0, ib = 0;
     if (live) {
-        ia = src[2L * b * N + 2 * k];
-        ib = src[2L * b * N + 2 * k + 1];
+        ia = clamp_row(src[2L * b * N + 2 * k], nx);
+        ib = clamp_row(src[2L * b * N + 2 * k + 1], nx);
     }
     const uint8_t* xa = ximg + (long)ia * rowbytes;
     const uint8_t* xb = ximg + (long)ib * rowbytes;
@@ -232,6 +226,7 @@ __global__ __launch_bounds__(kRowThreads) void unmerge_kernel(
     const long rowbytes = (long)D * S::kBytes;
     const int vpr = (int)(rowbytes / 16);
     const uint8_t* zimg = z + (long)(z_off ? z_off[b] : b * N) * rowbytes;
+    const int nz = z_off ? z_off[b + 1] - z_off[b] : N;  // rows of z for image b: a map entry past them reads zeros
     const int32_t* mapb = map + (long)b * N;
     const int32_t* map2b = map2 ? map2 + (long)b * N : nullptr;
     uint8_t* oimg = out + (long)b * rows * rowbytes;
@@ -244,7 +239,7 @@ __global__ __launch_bounds__(kRowThreads) void unmerge_kernel(
                 if (map_ab) map_ab[(long)b * N + r - E] = m;
             }
         }
-        src_row[r - r0] = m;
+        src_row[r - r0] = m < nz ? m : -1;
     }
     __syncthreads();
     for_each_vec_batched<kGatherBatch>((long)r0 * vpr, (long)r1 * vpr, vpr,
@@ -269,8 +264,8 @@ int rows_per_block_for(long rowbytes, long block_bytes = kRowBytesPerBlock)
 
 }  // namespace
 
-hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* count,
-                               int B, int N, int D, int dt, void* y, int32_t* y_off, hipStream_t stream, float* y_inv)
+hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* y_off, int B,
+                               int N, int D, int dt, void* y, float* y_inv, hipStream_t stream)
 {
     const long rowbytes = (long)D * (dt == kBf16 ? 2 : 4);
     const int rpb = rows_per_block_for(rowbytes);
@@ -282,18 +277,18 @@ hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_
         const dim3 igrid((N + rows - 1) / rows, B);
         if (dt == kBf16)
             hipLaunchKernelGGL(pair_average_inv_kernel<Bf16>, igrid, dim3(kRowThreads), 0, stream, xp, x_off, src,
-                               count, N, D, yp, y_off, y_inv);
+                               y_off, N, D, yp, y_inv);
         else
             hipLaunchKernelGGL(pair_average_inv_kernel<F32>, igrid, dim3(kRowThreads), 0, stream, xp, x_off, src,
-                               count, N, D, yp, y_off, y_inv);
+                               y_off, N, D, yp, y_inv);
         return hipGetLastError();
     }
     if (dt == kBf16)
-        hipLaunchKernelGGL(pair_average_kernel<Bf16>, grid, dim3(kRowThreads), 0, stream, xp, x_off, src, count, N, D,
-                           rpb, yp, y_off);
+        hipLaunchKernelGGL(pair_average_kernel<Bf16>, grid, dim3(kRowThreads), 0, stream, xp, x_off, src, y_off, N, D,
+                           rpb, yp);
     else
-        hipLaunchKernelGGL(pair_average_kernel<F32>, grid, dim3(kRowThreads), 0, stream, xp, x_off, src, count, N, D,
-                           rpb, yp, y_off);
+        hipLaunchKernelGGL(pair_average_kernel<F32>, grid, dim3(kRowThreads), 0, stream, xp, x_off, src, y_off, N, D,
+                           rpb, yp);
     return hipGetLastError();
 }
 

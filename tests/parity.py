@@ -41,6 +41,7 @@ class StageReport:
     flipped_rows: int           # rows where the GPU chose another (accepted) neighbour
     max_feature_rel_err: float
     notes: list = field(default_factory=list)
+    oracle_nearest: object = None  # the oracle's Nearest on this stage's input
 
 
 def check_nearest(x64: np.ndarray, nb_gpu: np.ndarray, threads=None):
@@ -81,29 +82,68 @@ def image_rows(y: torch.Tensor, y_off: torch.Tensor, b: int) -> torch.Tensor:
     return y[int(off[b]):int(off[b + 1])]
 
 
+@dataclass
+class HostSchedule:
+    """A GPU schedule result copied to the host once (float64 rows)."""
+    nb: list        # per stage: int32 [B, N]
+    map: list       # per stage: int32 [B, N]
+    y: list         # per stage: float64 [rows, D] (packed)
+    y_off: list     # per stage: int64 [B+1]
+    rstar: np.ndarray
+    out: np.ndarray  # float64 [B, N, D]
+
+
+def to_host(res) -> HostSchedule:
+    return HostSchedule([st.nb.cpu().numpy() for st in res.stages], [st.map.cpu().numpy() for st in res.stages],
+                        [to64(st.y[: int(st.y_off[-1])]) for st in res.stages],
+                        [st.y_off.cpu().numpy().astype(np.int64) for st in res.stages],
+                        res.rstar.cpu().numpy(), to64(res.out))
+
+
 def check_schedule_image(x_img: torch.Tensor, dtype: str, res, b: int, threads=None):
-    """Full stage-local + end-to-end check of image b of a GPU run_schedule result."""
+    """Full stage-local + end-to-end check of image b of a GPU run_schedule result
+    (or of its HostSchedule copy)."""
+    h = res if isinstance(res, HostSchedule) else to_host(res)
     reports = []
-    cur = to64(x_img)
-    maps = []
-    for s, st in enumerate(res.stages):
-        nb_gpu = st.nb[b].cpu().numpy()[: cur.shape[0]]
-        map_gpu = st.map[b].cpu().numpy()
-        y_gpu = to64(image_rows(st.y, st.y_off, b))
-        reports.append(check_stage(cur, dtype, nb_gpu, map_gpu, y_gpu, threads))
-        maps.append(map_gpu[: cur.shape[0]])
+    x0 = to64(x_img)
+    cur = x0
+    maps, inputs, nns = [], [], []
+    for s in range(len(h.nb)):
+        nb_gpu = h.nb[s][b, : cur.shape[0]]
+        map_gpu = h.map[s][b]
+        y_gpu = h.y[s][h.y_off[s][b]:h.y_off[s][b + 1]]
+        n = cur.shape[0]
+        nn, flips, near = check_nearest(cur, nb_gpu, threads)
+        ref = oracle.merge(cur, dtype, nb=nb_gpu)
+        assert np.array_equal(map_gpu[:n], ref.map), f"stage {s + 1}: merge map differs from the oracle seeded with the GPU nb"
+        assert np.all(map_gpu[n:] == -1), "map entries beyond n_b must be -1"
+        assert y_gpu.shape[0] == ref.count, f"count {y_gpu.shape[0]} vs oracle {ref.count}"
+        err = rel_err(y_gpu, ref.y)
+        assert err <= FEATURE_RTOL[dtype], f"merged features: max relative error {err:.3e}"
+        reports.append(StageReport(n, ref.count, near, flips, err, oracle_nearest=nn))
+        maps.append(map_gpu[:n])
+        inputs.append(cur)
+        nns.append(nn)
         cur = y_gpu
     # Composition and reconstruction: bit-exact given the GPU's own maps.
     rstar = maps[0]
     for m in maps[1:]:
         rstar = oracle.compose(rstar, m)
-    got_r = res.rstar[b].cpu().numpy()
+    got_r = h.rstar[b]
     assert np.array_equal(got_r, rstar), "composed map differs"
-    got_out = to64(res.out[b])
+    got_out = h.out[b]
     assert np.array_equal(got_out, oracle.unmerge(cur, rstar)), "reconstruction is not the gather"
-    # End to end: with no accepted flips the whole chain equals the oracle's from X.
+    # End to end: with no accepted flips the whole chain equals the oracle's from X. The
+    # oracle's own chain is run stage by stage; where its stage input is bitwise the GPU's,
+    # the nearest neighbours the stage-local check computed on that input are reused.
     if all(r.flipped_rows == 0 for r in reports):
-        stages, r_ref, up_ref = oracle.schedule(to64(x_img), dtype, insertions=len(res.stages), threads=threads)
+        ref_cur, r_ref = x0, None
+        for s in range(len(h.nb)):
+            same = ref_cur.shape == inputs[s].shape and np.array_equal(ref_cur, inputs[s])
+            st = oracle.merge(ref_cur, dtype, threads, nb=nns[s].nb if same else None)
+            r_ref = st.map.copy() if r_ref is None else oracle.compose(r_ref, st.map)
+            ref_cur = st.y
         assert np.array_equal(got_r, r_ref), "end-to-end composed map differs"
-        assert rel_err(got_out, up_ref) <= FEATURE_RTOL[dtype], "end-to-end reconstruction differs"
+        assert rel_err(got_out, oracle.unmerge(ref_cur, r_ref)) <= FEATURE_RTOL[dtype], \
+            "end-to-end reconstruction differs"
     return reports

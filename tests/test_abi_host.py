@@ -34,59 +34,83 @@ def test_version_and_status_strings(lib):
 
 def test_workspace_bytes_and_offsets(lib):
     r = lambda v: (v + 255) // 256 * 256
+    sync = r(4 * 65536)  # MPM_MAX_B + 1 arrival counters, at offset 0 for every shape
     for B, N in [(64, 1024), (16, 4096), (3, 5), (1, 257)]:
         T = (N + 63) // 64  # partial slots per token, include/mpm.h
-        want = r(4 * B * N) + r(8 * B * N) + r(4 * B) + r(4 * B * T * N) + r(4 * B * T * N)
+        want = sync + r(4 * B * N) + r(8 * B * N) + r(4 * B * T * N) + r(4 * B * T * N)
         assert lib.mpm_workspace_bytes(B, N) == want
         off = _lib.workspace_offsets(B, N)
-        assert off["nb"] == 0 and off["src"] == r(4 * B * N) and off["count"] == off["src"] + r(8 * B * N)
-        assert off["pv"] == off["count"] + r(4 * B) and off["pi"] == off["pv"] + r(4 * B * T * N)
+        assert off["sync"] == 0 and off["nb"] == sync and off["src"] == sync + r(4 * B * N)
+        assert off["pv"] == off["src"] + r(8 * B * N) and off["pi"] == off["pv"] + r(4 * B * T * N)
         assert all(v % 256 == 0 for v in off.values())
     assert lib.mpm_workspace_bytes(0, 5) == 0
     assert lib.mpm_workspace_offsets(0, 5, None, None, None, None, None) == 1
 
 
+def test_workspace_init_rejects(lib):
+    """Argument errors of mpm_workspace_init, returned before any launch."""
+    assert lib.mpm_workspace_init(None, 1 << 20, None) == 1                       # NULL
+    assert lib.mpm_workspace_init(ctypes.c_void_p(0x10010), 1 << 20, None) == 1   # not 256-byte aligned
+    assert lib.mpm_workspace_init(A, 4 * 65536 - 1, None) == 3                    # smaller than the sync region
+
+
+AUTO = 0
+
+
 @pytest.mark.parametrize("args,code", [
-    ((A, None, 0, 16, 64, 1, A2, None), 1),         # B < 1
-    ((A, None, 2, 0, 64, 1, A2, None), 1),          # N < 1
-    ((A, None, 2, 16, 0, 1, A2, None), 1),          # D < 1
-    ((A, None, 2, 16, 12, 1, A2, None), 1),         # bf16 rows not 16-byte multiples
-    ((A, None, 2, 16, 6, 0, A2, None), 1),          # f32 rows not 16-byte multiples
-    ((A, None, 2, 16, 64, 7, A2, None), 1),         # unknown dtype
-    ((None, None, 2, 16, 64, 1, A2, None), 1),      # null tokens
-    ((MIS, None, 2, 16, 64, 1, A2, None), 1),       # misaligned tokens
-    ((A, None, 2, 16, 64, 1, None, None), 1),       # null nb
-    ((A, None, 2, 16384 + 1, 64, 1, A2, None), 2),  # N above MPM_MAX_N
-    ((A, None, 65536, 16, 64, 1, A2, None), 2),     # B above MPM_MAX_B
-    ((A, None, 2, 16, 16384 + 8, 1, A2, None), 2),  # D above MPM_MAX_D
+    ((A, None, 0, 16, 64, 1, AUTO, A2, None), 1),         # B < 1
+    ((A, None, 2, 0, 64, 1, AUTO, A2, None), 1),          # N < 1
+    ((A, None, 2, 16, 0, 1, AUTO, A2, None), 1),          # D < 1
+    ((A, None, 2, 16, 12, 1, AUTO, A2, None), 1),         # bf16 rows not 16-byte multiples
+    ((A, None, 2, 16, 6, 0, AUTO, A2, None), 1),          # f32 rows not 16-byte multiples
+    ((A, None, 2, 16, 64, 7, AUTO, A2, None), 1),         # unknown dtype
+    ((A, None, 2, 16, 64, 1, 4, A2, None), 1),            # unknown schedule
+    ((A, None, 2, 16, 64, 1, -1, A2, None), 1),           # unknown schedule
+    ((None, None, 2, 16, 64, 1, AUTO, A2, None), 1),      # null tokens
+    ((MIS, None, 2, 16, 64, 1, AUTO, A2, None), 1),       # misaligned tokens
+    ((A, None, 2, 16, 64, 1, AUTO, None, None), 1),       # null nb
+    ((A, None, 2, 16384 + 1, 64, 1, AUTO, A2, None), 2),  # N above MPM_MAX_N
+    ((A, None, 65536, 16, 64, 1, AUTO, A2, None), 2),     # B above MPM_MAX_B
+    ((A, None, 2, 16, 16384 + 8, 1, AUTO, A2, None), 2),  # D above MPM_MAX_D
 ])
 def test_argmax_rejects(lib, args, code):
     big = 1 << 40
     assert lib.mpm_argmax(*args, A, big, None) == code
-    if args[6] is not None:  # the same rejection holds for the affinity step (which takes no nb)
-        assert lib.mpm_affinity(*args[:6], A, big, None) == code
+    if args[7] is not None:  # the same rejection holds for the affinity steps (which take no nb)
+        x, x_off, B, N, D, dt, sch = args[:7]
+        assert lib.mpm_affinity(x, x_off, None, B, N, D, dt, sch, A, big, None, None, None) == code
+        assert lib.mpm_affinity_compact(x, x_off, None, B, N, D, dt, sch, A2, A2, A, big, None, None, None) == code
+        assert lib.mpm_merge(x, x_off, None, B, N, D, dt, sch, A2, A2, None, A2, A, big, None) == code
 
 
 def test_workspace_checks(lib):
     need = lib.mpm_workspace_bytes(4, 64)
-    ok = (A, None, 4, 64, 64, 1, A2, A2, A2, A, need)
     # Workspace one byte short.
-    assert lib.mpm_merge(*ok[:10], need - 1, None) == 3
-    assert lib.mpm_affinity(A, None, 4, 64, 64, 1, A, need - 1, None) == 3
-    assert lib.mpm_argmax(A, None, 4, 64, 64, 1, A2, None, A, need - 1, None) == 3
-    assert lib.mpm_pair_compact_ws(None, 4, 64, 64, 1, A2, A, need - 1, None) == 3
+    assert lib.mpm_merge(A, None, None, 4, 64, 64, 1, AUTO, A2, A2, None, A2, A, need - 1, None) == 3
+    assert lib.mpm_affinity(A, None, None, 4, 64, 64, 1, AUTO, A, need - 1, None, None, None) == 3
+    assert lib.mpm_affinity_compact(A, None, None, 4, 64, 64, 1, AUTO, A2, A2, A, need - 1, None, None, None) == 3
+    assert lib.mpm_argmax(A, None, 4, 64, 64, 1, AUTO, A2, None, A, need - 1, None) == 3
     # Workspace not 256-byte aligned, or missing.
-    assert lib.mpm_merge(*ok[:9], ctypes.c_void_p(0x10010), need, None) == 1
-    assert lib.mpm_merge(*ok[:9], None, need, None) == 1
-    assert lib.mpm_affinity(A, None, 4, 64, 64, 1, None, need, None) == 1
-    # Null merged-token buffer.
-    assert lib.mpm_merge(A, None, 4, 64, 64, 1, None, A2, A2, A, need, None) == 1
+    assert lib.mpm_merge(A, None, None, 4, 64, 64, 1, AUTO, A2, A2, None, A2, ctypes.c_void_p(0x10010), need,
+                         None) == 1
+    assert lib.mpm_merge(A, None, None, 4, 64, 64, 1, AUTO, A2, A2, None, A2, None, need, None) == 1
+    assert lib.mpm_affinity(A, None, None, 4, 64, 64, 1, AUTO, None, need, None, None, None) == 1
+    # Null merged-token buffer, offsets or map.
+    assert lib.mpm_merge(A, None, None, 4, 64, 64, 1, AUTO, None, A2, None, A2, A, need, None) == 1
+    assert lib.mpm_merge(A, None, None, 4, 64, 64, 1, AUTO, A2, None, None, A2, A, need, None) == 1
+    assert lib.mpm_merge(A, None, None, 4, 64, 64, 1, AUTO, A2, A2, None, None, A, need, None) == 1
+    assert lib.mpm_affinity_compact(A, None, None, 4, 64, 64, 1, AUTO, None, A2, A, need, None, None, None) == 1
+    assert lib.mpm_affinity_compact(A, None, None, 4, 64, 64, 1, AUTO, A2, None, A, need, None, None, None) == 1
 
 
 def test_other_entry_points_reject(lib):
     assert lib.mpm_pair_compact(A, None, 0, 8, A, A, A, None) == 1
     assert lib.mpm_pair_compact(None, None, 2, 8, A, A, A, None) == 1
-    assert lib.mpm_pair_average(A, None, A, A, 2, 8, 64, 1, MIS, A, None) == 1
+    assert lib.mpm_pair_compact(A, None, 2, 8, A, A, None, None) == 1            # y_off NULL
+    assert lib.mpm_pair_average(A, None, A, A, 2, 8, 64, 1, MIS, None, None) == 1  # y misaligned
+    assert lib.mpm_pair_average(A, None, A, None, 2, 8, 64, 1, A2, None, None) == 1  # y_off NULL
+    assert lib.mpm_pair_average(A, None, A, A, 2, 8, 63, 1, A2, None, None) == 1   # D % 8 (bf16)
+    assert lib.mpm_pair_average(A, None, A, A, 2, 8, 64, 1, A2, ctypes.c_void_p(0x20002), None) == 1  # y_inv
     assert lib.mpm_compose(A, None, 2, 8, A, None) == 1
     assert lib.mpm_compose(A, A, 2, 16385, A, None) == 2
     assert lib.mpm_unmerge(A, None, A, None, -1, 2, 8, 64, 1, A, None) == 1   # E < 0
@@ -103,47 +127,30 @@ def test_other_entry_points_reject(lib):
     assert lib.mpm_last_hip_error() == 0
 
 
-def test_given_norm_entry_points_reject(lib):
-    """mpm_affinity_inv and mpm_pair_average_inv: the checks of their plain
-    versions, plus the norm pointer, and rows the norm-taking kernels do not cover."""
+def test_given_norms_reject(lib):
+    """Given inverse norms: a misaligned pointer, and rows the norm-taking kernels do
+    not cover, are rejected by every affinity entry point."""
     ws = ctypes.c_size_t(1 << 30)
-    assert lib.mpm_affinity_inv(A, None, None, 2, 8, 64, 1, A2, ws, None, None, None) == 1      # x_inv NULL
-    assert lib.mpm_affinity_inv(A, None, ctypes.c_void_p(0x10002), 2, 8, 64, 1, A2, ws, None, None, None) == 1
-    assert lib.mpm_affinity_inv(MIS, None, A, 2, 8, 64, 1, A2, ws, None, None, None) == 1       # x misaligned
-    assert lib.mpm_affinity_inv(A, None, A, 0, 8, 64, 1, A2, ws, None, None, None) == 1         # B < 1
-    assert lib.mpm_affinity_inv(A, None, A, 2, 8, 40, 1, A2, ws, None, None, None) == 2         # 80-byte rows
-    assert lib.mpm_affinity_inv(A, None, A, 2, 8, 8, 0, A2, ws, None, None, None) == 2          # 32-byte rows
-    assert lib.mpm_affinity_inv(A, None, A, 2, 8, 64, 0, A2, ws, None, None, None) == 2         # float32 rows
-    assert lib.mpm_affinity_inv(A, None, A, 2, 8, 64, 1, A2, 16, None, None, None) == 3         # workspace
-    assert lib.mpm_pair_average_inv(A, None, A, A, 2, 8, 64, 1, A2, A, None, None) == 1         # y_inv NULL
-    assert lib.mpm_pair_average_inv(A, None, A, A, 2, 8, 64, 1, MIS, A, A, None) == 1           # y misaligned
-    assert lib.mpm_pair_average_inv(A, None, A, A, 2, 8, 63, 1, A2, A, A, None) == 1            # D % 8 (bf16)
+    bad = ctypes.c_void_p(0x10002)
+    for D, dt, code in [(64, 1, 1), (40, 1, 2), (8, 1, 2), (64, 0, 2)]:  # misaligned; 80-, 16-byte, f32 rows
+        ptr = bad if code == 1 else A
+        assert lib.mpm_affinity(A, None, ptr, 2, 8, D, dt, AUTO, A2, ws, None, None, None) == code
+        assert lib.mpm_affinity_compact(A, None, ptr, 2, 8, D, dt, AUTO, A2, A2, A2, ws, None, None, None) == code
+        assert lib.mpm_merge(A, None, ptr, 2, 8, D, dt, AUTO, A2, A2, None, A2, A2, ws, None) == code
+    assert lib.mpm_affinity(MIS, None, A, 2, 8, 64, 1, AUTO, A2, ws, None, None, None) == 1      # x misaligned
+    assert lib.mpm_affinity(A, None, A, 2, 8, 64, 1, AUTO, A2, 16, None, None, None) == 3        # workspace
     assert lib.mpm_last_hip_error() == 0
 
 
-def test_affinity_schedule_knob(lib):
-    """Host-only: the schedule setter returns the previous mode, accepts the four
-    mpm_schedule values and rejects anything else without changing the mode."""
-    prev = lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_FULL)
-    try:
-        assert prev in (_lib.MPM_SCHEDULE_AUTO, _lib.MPM_SCHEDULE_FULL, _lib.MPM_SCHEDULE_SYMMETRIC,
-                        _lib.MPM_SCHEDULE_FULL_64)
-        assert lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_SYMMETRIC) == _lib.MPM_SCHEDULE_FULL
-        assert lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_FULL_64) == _lib.MPM_SCHEDULE_SYMMETRIC
-        for bad in (-1, 4, 1 << 20):
-            assert lib.mpm_set_affinity_schedule(bad) == -1
-        assert lib.mpm_set_affinity_schedule(_lib.MPM_SCHEDULE_AUTO) == _lib.MPM_SCHEDULE_FULL_64
-    finally:
-        lib.mpm_set_affinity_schedule(prev)
+def test_schedule_query_rejects(lib):
+    """The schedule is an argument of every affinity call (the library holds no mode);
+    the query rejects bad sizes, unknown schedules and a NULL output without writing it."""
     out = ctypes.c_int32(-7)
-    assert lib.mpm_affinity_schedule_used(0, 1024, 768, 1, ctypes.byref(out)) == _lib.MPM_ERR_INVALID_ARG
-    assert lib.mpm_affinity_schedule_used(64, 1024, 768, 1, None) == _lib.MPM_ERR_INVALID_ARG
+    assert lib.mpm_affinity_schedule_used(0, 1024, 768, 1, AUTO, ctypes.byref(out)) == _lib.MPM_ERR_INVALID_ARG
+    assert lib.mpm_affinity_schedule_used(64, 1024, 768, 1, 9, ctypes.byref(out)) == _lib.MPM_ERR_INVALID_ARG
+    assert lib.mpm_affinity_schedule_used(64, 1024, 768, 1, AUTO, None) == _lib.MPM_ERR_INVALID_ARG
     assert out.value == -7
+    assert not hasattr(lib, "mpm_set_affinity_schedule") or "mpm_set_affinity_schedule" not in _lib.header_functions()
     import paper_2604_05718_amd as mpm
-    before = mpm.set_affinity_schedule("full")
-    try:
-        assert mpm.set_affinity_schedule("symmetric") == "full"
-        with pytest.raises(ValueError):
-            mpm.set_affinity_schedule("diagonal")
-    finally:
-        mpm.set_affinity_schedule(before)
+    with pytest.raises(ValueError):
+        mpm.affinity_schedule_used(64, 1024, 768, __import__("torch").bfloat16, "diagonal")

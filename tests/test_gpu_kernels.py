@@ -132,9 +132,11 @@ def test_pair_compact_bitexact(N):
     for b, n in enumerate(ns):
         nb[b, :n] = random_nb(rng, n)
     off = torch.from_numpy(np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)).to(DEV)
-    m, src, count = mpm.pair_compact(torch.from_numpy(nb).to(DEV), x_off=off)
+    m, src, y_off = mpm.pair_compact(torch.from_numpy(nb).to(DEV), x_off=off)
     torch.cuda.synchronize()
-    m, src, count = m.cpu().numpy(), src.cpu().numpy(), count.cpu().numpy()
+    m, src, y_off = m.cpu().numpy(), src.cpu().numpy(), y_off.cpu().numpy()
+    count = np.diff(y_off)
+    assert y_off[0] == 0
     for b, n in enumerate(ns):
         pr = oracle.pairs(nb[b, :n])
         assert count[b] == pr.count
@@ -158,8 +160,8 @@ def test_pair_average(dtype, D):
     for b, n in enumerate(ns):
         nb[b, :n] = random_nb(rng, n)
         prs.append(oracle.pairs(nb[b, :n]))
-    m, src, count = mpm.pair_compact(torch.from_numpy(nb).to(DEV), x_off=x_off)
-    y, y_off = mpm.pair_average(x, src, count, x_off=x_off, N=N)
+    m, src, y_off = mpm.pair_compact(torch.from_numpy(nb).to(DEV), x_off=x_off)
+    y = mpm.pair_average(x, src, y_off, x_off=x_off, N=N)
     torch.cuda.synchronize()
     off = y_off.cpu().numpy()
     assert off.tolist() == [0] + np.cumsum([p.count for p in prs]).tolist()
@@ -174,7 +176,7 @@ def test_pair_average(dtype, D):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("D", [8, 64, 768, 2048, 2056, 16384])
 def test_pair_average_inverse_norms(dtype, D):
-    """mpm_pair_average_inv: the same merged rows as mpm_pair_average, bit for bit,
+    """mpm_pair_average with y_inv: the same merged rows as without, bit for bit,
     on rows of 16 bytes to 64 KB (1 to 4096 vectors of 16 bytes: 1 to 64 lanes per
     row, one or several batches of vectors per lane, a ragged last batch),
     and 1 / max(||y_k||, 1e-12) of every merged row against float64 norms of the
@@ -193,13 +195,12 @@ def test_pair_average_inverse_norms(dtype, D):
     for b, n in enumerate(ns):
         nb[b, :n] = random_nb(rng, n)
     nb[1, 3] = -1 if ns[1] == 1 else nb[1, 3]
-    m, src, count = mpm.pair_compact(torch.from_numpy(nb).to(DEV), x_off=x_off)
-    y, y_off = mpm.pair_average(x, src, count, x_off=x_off, N=N)
-    y2, y_off2, inv = mpm.pair_average(x, src, count, x_off=x_off, N=N, with_inv=True)
-    _, _, inv2 = mpm.pair_average(x, src, count, x_off=x_off, N=N, with_inv=True)
+    m, src, y_off = mpm.pair_compact(torch.from_numpy(nb).to(DEV), x_off=x_off)
+    y = mpm.pair_average(x, src, y_off, x_off=x_off, N=N)
+    y2, inv = mpm.pair_average(x, src, y_off, x_off=x_off, N=N, with_inv=True)
+    _, inv2 = mpm.pair_average(x, src, y_off, x_off=x_off, N=N, with_inv=True)
     torch.cuda.synchronize()
     total = int(y_off[B].item())
-    assert torch.equal(y_off, y_off2)
     assert torch.equal(y[:total].view(torch.int16 if dtype == "bf16" else torch.int32),
                        y2[:total].view(torch.int16 if dtype == "bf16" else torch.int32))
     assert torch.equal(inv[:total].view(torch.int32), inv2[:total].view(torch.int32))
@@ -355,8 +356,8 @@ def test_deterministic_across_runs():
 
 
 def test_step_entry_points_equal_merge_and_schedule():
-    """mpm_merge == mpm_affinity + mpm_pair_compact_ws + mpm_pair_average, and the
-    preallocated Schedule equals run_schedule, bit for bit (ragged stage 2)."""
+    """The preallocated Schedule (mpm_affinity_compact, then mpm_pair_average) equals
+    run_schedule (mpm_merge), bit for bit (ragged stage 2)."""
     from paper_2604_05718_amd import api
 
     rng = np.random.default_rng(21)
@@ -383,8 +384,7 @@ def test_step_entry_points_equal_merge_and_schedule():
 
 
 def test_timed_schedule_equals_untimed():
-    """Binding timing events to the affinity dispatches (mpm_affinity_timed)
-    changes no result, and each pair measures a positive kernel duration."""
+    """Binding timing events to the affinity dispatches changes no result, and each pair measures a positive kernel duration."""
     from paper_2604_05718_amd import api
 
     rng = np.random.default_rng(22)
@@ -473,21 +473,12 @@ def test_many_items_per_workgroup():
 
 # ---- symmetric affinity schedule ----------------------------------------------
 
-@pytest.fixture
-def schedule(request):
-    prev = mpm.set_affinity_schedule(request.param)
-    yield request.param
-    mpm.set_affinity_schedule(prev)
-
-
-def _affinity_partials(x2, x_off, B, N, D, dtype):
-    """Run mpm_affinity; return the partials (pv, pi) as [B, T, N] host arrays."""
+def _affinity_partials(x2, x_off, B, N, D, dtype, schedule, x_inv=None):
+    """Run mpm_affinity under a schedule (with given inverse norms x_inv, if any);
+    return the partials (pv, pi) as [B, T, N] host arrays."""
     from paper_2604_05718_amd import _lib
-    from paper_2604_05718_amd.api import _p, _stream
-    ws = torch.empty((mpm.workspace_bytes(B, N),), dtype=torch.uint8, device=DEV)
-    dt = _lib.MPM_BF16 if dtype == "bf16" else _lib.MPM_F32
-    _lib.check("mpm_affinity", _lib.load().mpm_affinity(_p(x2), _p(x_off), B, N, D, dt, _p(ws), ws.numel(),
-                                                        _stream()))
+    ws = mpm.affinity(x2, x_off, N=N, x_inv=x_inv, schedule=schedule) if x_off is not None else \
+        mpm.affinity(x2.view(B, N, D), x_inv=x_inv, schedule=schedule)
     torch.cuda.synchronize()
     o = _lib.workspace_offsets(B, N)
     T = (N + 63) // 64  # partial slots per token (the workspace layout of include/mpm.h)
@@ -554,24 +545,14 @@ def test_symmetric_schedule_partials_bit_identical(dtype, name):
     else:
         x2 = torch.stack(rows).to(DEV).view(B * N, D)
         x_off = None
-    out = {}
-    for mode in ("full", "symmetric"):
-        prev = mpm.set_affinity_schedule(mode)
-        try:
-            out[mode] = _affinity_partials(x2, x_off, B, N, D, dtype)
-        finally:
-            mpm.set_affinity_schedule(prev)
+    out = {mode: _affinity_partials(x2, x_off, B, N, D, dtype, mode) for mode in ("full", "symmetric")}
     (fv, fi), (sv, si) = out["full"], out["symmetric"]
     for b, n in enumerate(ns):
         tiles = (n + 255) // 256
         assert np.array_equal(fv[b, :tiles, :n].view(np.uint32), sv[b, :tiles, :n].view(np.uint32)), b
         assert np.array_equal(fi[b, :tiles, :n], si[b, :tiles, :n]), b
-    prev = mpm.set_affinity_schedule("symmetric")
-    try:
-        nb = mpm.argmax(x2 if packed else x2.view(B, N, D), x_off=x_off, N=N if packed else None)
-        torch.cuda.synchronize()
-    finally:
-        mpm.set_affinity_schedule(prev)
+    nb = mpm.argmax(x2 if packed else x2.view(B, N, D), x_off=x_off, N=N if packed else None, schedule="symmetric")
+    torch.cuda.synchronize()
     nb = nb.cpu().numpy()
     for b, n in enumerate(ns):
         if n == 1:
@@ -582,27 +563,11 @@ def test_symmetric_schedule_partials_bit_identical(dtype, name):
         check_nearest(to64(rows[b]), nb[b, :n])
 
 
-def _affinity_inv_partials(x2, x_off, x_inv, B, N, D, dtype):
-    """Run mpm_affinity_inv; return the partials (pv, pi) as [B, T, N] host arrays."""
-    from paper_2604_05718_amd import _lib
-    from paper_2604_05718_amd.api import _p, _stream
-    ws = torch.empty((mpm.workspace_bytes(B, N),), dtype=torch.uint8, device=DEV)
-    dt = _lib.MPM_BF16 if dtype == "bf16" else _lib.MPM_F32
-    _lib.check("mpm_affinity_inv", _lib.load().mpm_affinity_inv(_p(x2), _p(x_off), _p(x_inv), B, N, D, dt, _p(ws),
-                                                                ws.numel(), None, None, _stream()))
-    torch.cuda.synchronize()
-    o = _lib.workspace_offsets(B, N)
-    T = (N + 63) // 64
-    pv = ws[o["pv"]:o["pv"] + 4 * B * T * N].view(torch.float32).view(B, T, N).cpu().numpy()
-    pi = ws[o["pi"]:o["pi"] + 4 * B * T * N].view(torch.int32).view(B, T, N).cpu().numpy()
-    return pv, pi
-
-
 @pytest.mark.parametrize("dtype", ["bf16"])
 @pytest.mark.parametrize("name", ["dense_777", "rows_192_bytes", "duplicated_rows", "all_equal", "packed_ragged",
                                   "deferred_packed"])
 def test_affinity_with_given_norms(dtype, name):
-    """mpm_affinity_inv with float64-exact inverse norms (rounded to float32): the
+    """mpm_affinity with float64-exact inverse norms (rounded to float32): the
     full and symmetric schedules give bit-identical partials, and the nearest
     neighbours reduced from them (larger score, then smaller index) pass the oracle
     check, ties included."""
@@ -620,13 +585,7 @@ def test_affinity_with_given_norms(dtype, name):
         x_off = None
         inv = np.concatenate([1.0 / np.maximum(np.sqrt((to64(r) ** 2).sum(axis=1)), 1e-12) for r in rows])
     x_inv = torch.from_numpy(inv.astype(np.float32)).to(DEV)
-    out = {}
-    for mode in ("full", "symmetric"):
-        prev = mpm.set_affinity_schedule(mode)
-        try:
-            out[mode] = _affinity_inv_partials(x2, x_off, x_inv, B, N, D, dtype)
-        finally:
-            mpm.set_affinity_schedule(prev)
+    out = {mode: _affinity_partials(x2, x_off, B, N, D, dtype, mode, x_inv=x_inv) for mode in ("full", "symmetric")}
     (fv, fi), (sv, si) = out["full"], out["symmetric"]
     for b, n in enumerate(ns):
         tiles = (n + 255) // 256
@@ -643,7 +602,7 @@ def test_affinity_with_given_norms(dtype, name):
         check_nearest(to64(rows[b]), nb)
 
 
-@pytest.mark.parametrize("schedule", ["full", "symmetric"], indirect=True)
+@pytest.mark.parametrize("schedule", ["full", "symmetric"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_merge_many_tiles_both_schedules(dtype, schedule):
     """The packed ragged merge with more than four candidate tiles per image,
@@ -655,7 +614,7 @@ def test_merge_many_tiles_both_schedules(dtype, schedule):
     off = np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)
     x = torch.cat(rows).to(DEV)
     print(f"merge many tiles {dtype} schedule={schedule}", flush=True)
-    res = mpm.merge(x, torch.from_numpy(off).to(DEV), N=N)
+    res = mpm.merge(x, torch.from_numpy(off).to(DEV), N=N, schedule=schedule)
     torch.cuda.synchronize()
     m = res.map.cpu().numpy()
     nb = res.nb.cpu().numpy()
@@ -702,14 +661,10 @@ def test_small_blocks_equal_full_schedule(dtype, name):
         x_off = None
     out = {}
     for mode in ("full", "full_64"):
-        prev = mpm.set_affinity_schedule(mode)
-        try:
-            assert mpm.affinity_schedule_used(B, N, D, x.dtype) == mode
-            nb, best = mpm.argmax(x, x_off=x_off, N=N if packed else None, with_best=True)
-            torch.cuda.synchronize()
-            out[mode] = (nb.cpu().numpy(), best.cpu().numpy())
-        finally:
-            mpm.set_affinity_schedule(prev)
+        assert mpm.affinity_schedule_used(B, N, D, x.dtype, mode) == mode
+        nb, best = mpm.argmax(x, x_off=x_off, N=N if packed else None, with_best=True, schedule=mode)
+        torch.cuda.synchronize()
+        out[mode] = (nb.cpu().numpy(), best.cpu().numpy())
     (fn, fb), (sn, sb) = out["full"], out["full_64"]
     for b, n in enumerate(ns):
         assert np.array_equal(fn[b, :n], sn[b, :n]), b
@@ -723,56 +678,14 @@ def test_small_blocks_equal_full_schedule(dtype, name):
 def test_small_blocks_chosen_for_small_batches():
     """Auto mode takes the 64 x 64 blocks when a batch has at most 32 blocks of
     256 x 256 (rows a multiple of 64 bytes), and the large blocks otherwise."""
-    prev = mpm.set_affinity_schedule("auto")
-    try:
-        assert mpm.affinity_schedule_used(1, 1024, 192, torch.float32) == "full_64"
-        assert mpm.affinity_schedule_used(2, 1024, 768, torch.bfloat16) == "full_64"
-        assert mpm.affinity_schedule_used(3, 1024, 768, torch.bfloat16) != "full_64"
-        assert mpm.affinity_schedule_used(1, 4096, 1024, torch.bfloat16) != "full_64"
-        assert mpm.affinity_schedule_used(1, 1024, 24, torch.bfloat16) == "full"  # 48-byte rows: no schedule choice
-    finally:
-        mpm.set_affinity_schedule(prev)
-
-
-def _affinity_us(x, B, N, D, reps=9):
-    """Median duration (microseconds) of mpm_affinity_timed over reps launches."""
-    from paper_2604_05718_amd import _lib
-    from paper_2604_05718_amd.api import _p, _stream
-    lib = _lib.load()
-    ws = torch.empty((mpm.workspace_bytes(B, N),), dtype=torch.uint8, device=DEV)
-    dt = _lib.MPM_BF16 if x.dtype == torch.bfloat16 else _lib.MPM_F32
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps + 1)]
-    for a, b in ev:  # torch creates the underlying events on first record
-        a.record()
-        b.record()
-    for a, b in ev:
-        _lib.check("mpm_affinity_timed", lib.mpm_affinity_timed(_p(x), None, B, N, D, dt, _p(ws), ws.numel(),
-                                                                a.cuda_event, b.cuda_event, _stream()))
-    torch.cuda.synchronize()
-    return float(np.median([a.elapsed_time(b) * 1e3 for a, b in ev[1:]]))
-
-
-def test_full_schedule_spreads_items():
-    """At B = 32, N = 1024, D = 384 (bf16) both 256 x 256 schedules hand every
-    workgroup slot about two items (full: 16 per image, symmetric: 10 per image,
-    on 32 slots per group of 4 images), so their launches take about as long.
-    Items enumerated over the workspace's partial slots (ceil(N / 64) per token)
-    instead of the 256-wide tiles left three quarters of the full schedule's
-    items empty and piled its real ones on a quarter of the slots (3x slower);
-    this guards the balance that parity tests cannot see."""
-    B, N, D = 32, 1024, 384
-    g = torch.Generator().manual_seed(11)
-    x = torch.randn((B, N, D), generator=g).to(torch.bfloat16).to(DEV)
-    us = {}
-    for mode in ("full", "symmetric"):
-        prev = mpm.set_affinity_schedule(mode)
-        try:
-            assert mpm.affinity_schedule_used(B, N, D, x.dtype) == mode
-            us[mode] = _affinity_us(x, B, N, D)
-        finally:
-            mpm.set_affinity_schedule(prev)
-    print(f"affinity B={B} N={N} D={D}: full {us['full']:.1f} us, symmetric {us['symmetric']:.1f} us", flush=True)
-    assert us["full"] < 1.6 * us["symmetric"], us
+    assert mpm.affinity_schedule_used(1, 1024, 192, torch.float32) == "full_64"
+    assert mpm.affinity_schedule_used(2, 1024, 768, torch.bfloat16) == "full_64"
+    assert mpm.affinity_schedule_used(3, 1024, 768, torch.bfloat16) != "full_64"
+    assert mpm.affinity_schedule_used(1, 4096, 1024, torch.bfloat16) != "full_64"
+    assert mpm.affinity_schedule_used(1, 1024, 24, torch.bfloat16) == "full"  # 48-byte rows: no schedule choice
+    # The schedule is per call: forcing one for a query changes nothing for the next.
+    assert mpm.affinity_schedule_used(64, 1024, 768, torch.bfloat16, "full") == "full"
+    assert mpm.affinity_schedule_used(64, 1024, 768, torch.bfloat16) == "symmetric"
 
 
 # ---- the largest sizes the C ABI accepts -----------------------------------------
@@ -818,3 +731,82 @@ def test_many_images():
         assert np.array_equal(maps[b], ref.map), b
         assert y_off[b + 1] - y_off[b] == ref.count, b
         assert rel_err(y[y_off[b]:y_off[b + 1]], ref.y) <= 2e-2, b
+
+
+# ---- the affinity + compaction step ----------------------------------------------------
+
+def _step_case(name):
+    """(rows per image, N, D, dtype, schedule, packed) of the affinity + compaction cases."""
+    rng = np.random.default_rng(zlib.crc32(("step-" + name).encode()))
+    if name == "symmetric_deferred":  # 90 images: the half-block second launch
+        return [store(clustered(rng, 1024, 64, k=25), "bf16") for _ in range(90)], 1024, 64, "bf16", "symmetric", False
+    if name == "symmetric_packed":  # ragged images, duplicated rows (exact ties) in every fourth
+        sizes = [1024, 1000, 769, 768, 513, 256, 1, 900]
+        imgs = []
+        for b in range(88):
+            n = sizes[b % len(sizes)]
+            h = clustered(rng, (n + 1) // 2, 64, k=20) if b % 4 == 3 else clustered(rng, n, 64, k=25)
+            imgs.append(store(np.repeat(h, 2, axis=0)[:n] if b % 4 == 3 else h, "bf16"))
+        return imgs, 1024, 64, "bf16", "symmetric", True
+    if name == "full_f32":
+        return [store(clustered(rng, 700, 64, k=20), "f32") for _ in range(20)], 700, 64, "f32", "full", False
+    if name == "full_64_one_image":
+        return [store(clustered(rng, 1024, 64, k=12), "f32")], 1024, 64, "f32", "full_64", False
+    if name == "rows_48_bytes":  # bf16 rows of 48 bytes: the staged kernel (one partial per token)
+        return [store(clustered(rng, 300, 24, k=10), "bf16") for _ in range(3)], 300, 24, "bf16", "auto", False
+    if name == "rows_192_bytes":  # the 64-byte-chunk ring
+        return [store(clustered(rng, 777, 96, k=30), "bf16") for _ in range(12)], 777, 96, "bf16", "symmetric", False
+    if name == "many_images":  # 20000 images of 4 tokens: the images-done counter runs to 20000
+        return [store(rng.standard_normal((4, 32)), "bf16") for _ in range(20000)], 4, 32, "bf16", "auto", False
+    raise KeyError(name)
+
+
+@pytest.mark.parametrize("name", ["symmetric_deferred", "symmetric_packed", "full_f32", "full_64_one_image",
+                                  "rows_48_bytes", "rows_192_bytes", "many_images"])
+def test_affinity_compact_equals_argmax_then_compact(name):
+    """mpm_affinity_compact (partials reduced inside the compaction kernel, or by the
+    parallel reduction for many tiles; the workgroup that finishes the last image turns
+    the counts into offsets) gives the same nb, map, src and offsets, bit for bit, as
+    mpm_argmax followed by mpm_pair_compact (offsets by a second launch) on the same
+    input and schedule; the arrival counters are zero again after the call, and a
+    second call on the same workspace repeats the result."""
+    from paper_2604_05718_amd import _lib, api
+
+    rows, N, D, dtype, schedule, packed = _step_case(name)
+    ns = [r.shape[0] for r in rows]
+    B = len(rows)
+    print(f"affinity + compaction {name}: B={B} N={N} D={D} {dtype} schedule={schedule}", flush=True)
+    if packed:
+        x = torch.cat(rows).to(DEV)
+        x_off = torch.from_numpy(np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)).to(DEV)
+    else:
+        x = torch.stack(rows).to(DEV)
+        x_off = None
+    nb_ref = mpm.argmax(x, x_off=x_off, N=N, schedule=schedule)
+    m_ref, src_ref, off_ref = mpm.pair_compact(nb_ref, x_off=x_off)
+    ws = api.new_workspace(B, N, DEV)
+    x2 = x if packed else x.view(B * N, D)
+    got = []
+    for rep in range(2):
+        m = torch.full((B, N), -9, dtype=torch.int32, device=DEV)
+        y_off = torch.full((B + 1,), -9, dtype=torch.int32, device=DEV)
+        _lib.check("mpm_affinity_compact", _lib.load().mpm_affinity_compact(
+            api._p(x2), api._p(x_off), None, B, N, D, api._dt(x), api._sched(schedule), api._p(m), api._p(y_off),
+            api._p(ws), ws.numel(), None, None, api._stream()))
+        torch.cuda.synchronize()
+        sync = ws[: 4 * 65536].view(torch.int32)
+        assert int(torch.count_nonzero(sync)) == 0, f"call {rep}: arrival counters not reset"
+        got.append((m.clone(), y_off.clone(), api.ws_view(ws, B, N, "nb").clone(), api.ws_view(ws, B, N, "src").clone()))
+    for m, y_off, nb, src in got:
+        assert torch.equal(y_off, off_ref)
+        assert torch.equal(m, m_ref)
+        off = off_ref.cpu().numpy()
+        nbh, nbr, srch, srcr = nb.cpu().numpy(), nb_ref.cpu().numpy(), src.cpu().numpy(), src_ref.cpu().numpy()
+        for b, n in enumerate(ns):
+            assert np.array_equal(nbh[b, :n], nbr[b, :n]), b
+            c = off[b + 1] - off[b]
+            assert np.array_equal(srch[b, :c], srcr[b, :c]), b
+    # The neighbours themselves against the oracle, on a sample of images.
+    nbh = got[0][2].cpu().numpy()
+    for b in sorted({0, B // 2, B - 1}):
+        check_nearest(to64(rows[b]), nbh[b, :ns[b]])

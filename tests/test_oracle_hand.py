@@ -3,11 +3,13 @@
 Every expected value was derived by hand from the paper's definitions (Eq. 1-4,
 Sec. 3.2, Alg. 1), not produced by the oracle.
 """
+import os
+
 import numpy as np
 import pytest
 
 import oracle
-from golden_io import all_merge_cases, load
+from golden_io import GOLDEN, all_merge_cases, load
 
 
 @pytest.mark.parametrize("name", all_merge_cases())
@@ -95,3 +97,40 @@ def test_zero_token_goes_to_lowest_index():
     nn = oracle.nearest(x)
     assert nn.nb[1] == 0
     assert oracle.cosine(x, 1, 2) == 0.0
+
+
+def _unit(deg):
+    t = np.deg2rad(np.asarray(deg, dtype=np.float64))
+    return np.stack([np.cos(t), np.sin(t)], axis=1)
+
+
+def _top2_cases():
+    vals = {}
+    with open(os.path.join(GOLDEN, "top2_gap.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                k, _, v = line.partition(":")
+                vals[k.strip()] = [float(t) for t in v.split()]
+    return vals
+
+
+def test_top1_top2_hand_derived():
+    """The oracle's top-1 and top-2 cosines per row (the near-tie gap of the parity
+    protocol) against values derived by hand from angles: distinct maxima, a maximum
+    attained by every other row, a maximum attained twice or more, and a single
+    candidate (no second value). A wrong update on an equal maximum, a second value
+    left at -inf, or the maximum counted twice would fail one of them."""
+    c = _top2_cases()
+    for key in ("a", "c"):
+        nn = oracle.nearest(_unit(c[f"{key}_angles_deg"]))
+        np.testing.assert_allclose(nn.top1, np.cos(np.deg2rad(c[f"{key}_top1_deg"])), rtol=0, atol=1e-12)
+        np.testing.assert_allclose(nn.top2, np.cos(np.deg2rad(c[f"{key}_top2_deg"])), rtol=0, atol=1e-12)
+    n, d = (int(v) for v in c["b_onehot"])
+    nn = oracle.nearest(np.eye(n, d))
+    assert np.all(nn.top1 == 0.0) and np.all(nn.top2 == 0.0) and np.all(nn.gap == 0.0)
+    nn = oracle.nearest(_unit(c["d_angles_deg"]))
+    np.testing.assert_allclose(nn.top1, np.cos(np.deg2rad(c["d_top1_deg"])), rtol=0, atol=1e-12)
+    assert np.all(np.isneginf(nn.top2))
+    nn = oracle.nearest(_unit([30.0]))  # one token: no candidate at all
+    assert nn.nb[0] == -1 and np.isneginf(nn.top1[0]) and np.isneginf(nn.top2[0])
