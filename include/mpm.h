@@ -263,6 +263,25 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
               void* stream);
 
 /*
+ * mpm_merge for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the workspace
+ * is a file-scope device array of MPM_NOALLOC_SCRATCH_BYTES that each GPU the
+ * library runs on holds until the process ends; its address is looked up on the
+ * first call on a GPU, whose stream also gets one small fill kernel that clears
+ * its arrival counters. No call allocates or frees anything (no hipMalloc,
+ * hipFree or allocating library routine). Shapes whose mpm_workspace_bytes(B, N)
+ * exceed the array return MPM_ERR_WORKSPACE (B = 64 at N = 1024, B = 16 at
+ * N = 4096 and B = 32 at N = 2304 fit). Every call on a GPU shares that GPU's
+ * array and leaves its arrival counters zero, but its other contents are the last
+ * call's: calls that overlap on one GPU (several streams or threads) race and give
+ * wrong results, so order them. Arguments, results and other errors as mpm_merge
+ * (without the workspace, so nb and src are not readable).
+ */
+#define MPM_NOALLOC_SCRATCH_BYTES (48u << 20)
+int mpm_merge_noalloc(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D,
+                      int32_t dt, int32_t schedule, void* y, int32_t* y_off, float* y_inv, int32_t* map, void* stream);
+
+/*
  * Composition of merge maps (Eq. 3): map_ab[b*N + i] = map_b[b*N + map_a[b*N + i]],
  * or -1 where map_a[b*N + i] < 0. Both maps in slot layout; map_a's values
  * index image b's entries of map_b. map_ab may alias map_a.

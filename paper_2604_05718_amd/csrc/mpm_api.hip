@@ -4,6 +4,9 @@
 
 #include <stdint.h>
 
+#include <atomic>
+#include <mutex>
+
 
 #include "../../include/mpm.h"
 #include "mpm_launch.h"
@@ -138,6 +141,45 @@ hipError_t affinity_compact(const void* x, const int32_t* x_off, const float* x_
     return e;
 }
 
+// ---- workspace of the allocation-free entry point --------------------------------
+// A file-scope device array: each GPU the library runs on holds its own copy (at its
+// own address) until the process ends. In host code `scratch` names a host-side
+// stand-in, not device memory: its device address is looked up once per device with
+// hipGetSymbolAddress and only that address is ever passed to kernels or copies.
+constexpr size_t kScratchBytes = MPM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];  // device address of `scratch`, per device (set once)
+std::mutex g_scratch_mutex;
+
+// The device address of `scratch` on the current device. On the first call for a
+// device (with that device current) it is looked up, and the array's sync region is
+// cleared by a fill kernel on `st` (no memset node, so a first call under graph
+// capture records a kernel).
+hipError_t scratch_for_current_device(hipStream_t st, void** out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        std::lock_guard<std::mutex> lock(g_scratch_mutex);
+        p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+        if (p == nullptr) {
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return e;
+            if (p == nullptr) return hipErrorInvalidSymbol;
+            e = mpm::launch_zero_words(static_cast<int32_t*>(p), (long)kSyncWords, st);
+            if (e != hipSuccess) return e;
+            g_scratch_ptr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
+    return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -269,6 +311,25 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     const hipStream_t st = as_stream(stream);
     hipError_t e = affinity_compact(x, x_off, x_inv, B, N, D, dt, schedule, map, y_off, w, nullptr, nullptr, st);
+    if (e == hipSuccess) e = mpm::launch_pair_average(x, x_off, w.src, y_off, B, N, D, dt, y, y_inv, st);
+    return hip_status(e);
+}
+
+int mpm_merge_noalloc(const void* x, const int32_t* x_off, const float* x_inv, int32_t B, int32_t N, int32_t D,
+                      int32_t dt, int32_t schedule, void* y, int32_t* y_off, float* y_inv, int32_t* map, void* stream)
+{
+    int s = check_affinity(x, x_off, x_inv, B, N, D, dt, schedule);
+    if (s != MPM_OK) return s;
+    if (!ok_rows_ptr(y) || !ok_int_ptr(y_off) || !ok_opt_int_ptr(y_inv) || !ok_int_ptr(map))
+        return MPM_ERR_INVALID_ARG;
+    if (workspace_offsets(B, N).total > kScratchBytes) return MPM_ERR_WORKSPACE;
+    const hipStream_t st = as_stream(stream);
+    void* ws = nullptr;
+    hipError_t e = scratch_for_current_device(st, &ws);
+    if (e != hipSuccess) return hip_status(e);
+    Workspace w;
+    if ((s = carve(ws, kScratchBytes, B, N, &w)) != MPM_OK) return s;
+    e = affinity_compact(x, x_off, x_inv, B, N, D, dt, schedule, map, y_off, w, nullptr, nullptr, st);
     if (e == hipSuccess) e = mpm::launch_pair_average(x, x_off, w.src, y_off, B, N, D, dt, y, y_inv, st);
     return hip_status(e);
 }

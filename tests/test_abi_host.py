@@ -150,7 +150,23 @@ def test_schedule_query_rejects(lib):
     assert lib.mpm_affinity_schedule_used(64, 1024, 768, 1, 9, ctypes.byref(out)) == _lib.MPM_ERR_INVALID_ARG
     assert lib.mpm_affinity_schedule_used(64, 1024, 768, 1, AUTO, None) == _lib.MPM_ERR_INVALID_ARG
     assert out.value == -7
-    assert not hasattr(lib, "mpm_set_affinity_schedule") or "mpm_set_affinity_schedule" not in _lib.header_functions()
+    assert not hasattr(lib, "mpm_set_affinity_schedule")
     import paper_2604_05718_amd as mpm
     with pytest.raises(ValueError):
         mpm.affinity_schedule_used(64, 1024, 768, __import__("torch").bfloat16, "diagonal")
+
+
+def test_noalloc_rejects_before_any_device_use(lib):
+    """mpm_merge_noalloc: argument errors and shapes beyond its fixed device array are
+    rejected before the array is looked up (no GPU needed)."""
+    cap = 48 << 20
+    assert lib.mpm_workspace_bytes(64, 4096) > cap >= lib.mpm_workspace_bytes(16, 4096)
+    assert lib.mpm_workspace_bytes(64, 1024) <= cap and lib.mpm_workspace_bytes(32, 2304) <= cap
+    assert lib.mpm_merge_noalloc(A, None, None, 64, 4096, 64, 1, AUTO, A2, A2, None, A2, None) == 3
+    assert lib.mpm_merge_noalloc(A, None, None, 0, 16, 64, 1, AUTO, A2, A2, None, A2, None) == 1     # B < 1
+    assert lib.mpm_merge_noalloc(MIS, None, None, 2, 16, 64, 1, AUTO, A2, A2, None, A2, None) == 1   # x misaligned
+    assert lib.mpm_merge_noalloc(A, None, None, 2, 16, 64, 1, 9, A2, A2, None, A2, None) == 1        # schedule
+    assert lib.mpm_merge_noalloc(A, None, None, 2, 16, 64, 1, AUTO, None, A2, None, A2, None) == 1   # y NULL
+    assert lib.mpm_merge_noalloc(A, None, None, 2, 16, 64, 1, AUTO, A2, A2, None, None, None) == 1   # map NULL
+    assert lib.mpm_merge_noalloc(A, None, A, 2, 16, 64, 0, AUTO, A2, A2, None, A2, None) == 2        # f32 norms
+    assert lib.mpm_last_hip_error() == 0
