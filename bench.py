@@ -29,10 +29,13 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak"
 
 # HBM traffic of one affinity step (the whole-block launch and, where the schedule
-# defers diagonal blocks, the half-block launch) from rocprofv3 FETCH_SIZE / WRITE_SIZE
-# runs on this workload, calibrated with a copy kernel (profiles/). Valid only for
-# the kernel source it was measured on.
-TRAFFIC = {"source_sha256": "", "bytes_per_launch": None}
+# defers diagonal blocks, the half-block launch; the two insertions averaged) from
+# rocprofv3 FETCH_SIZE / WRITE_SIZE runs on each workload, calibrated with a copy
+# kernel (profiles/<workload>_rocprof.md). Valid only for the kernel source it was
+# measured on, with the default schedule.
+TRAFFIC = {"source_sha256": "d2f6621e8438d01006479306f60947d0499c50a2f6ad61b68431842fd9c56746",
+           "bytes_per_launch": {"vit_ti_512": 6555874, "vit_s_512": 24996198, "vit_b_512": 149457124,
+                                "vit_l_1024": 499851763, "stress_768": 178310894}}
 
 
 def log(*a):
@@ -139,6 +142,8 @@ def main() -> int:
                     help="budget of the CPU oracle baseline (0 skips it)")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="steps timed after evicting the caches (0 skips them)")
+    ap.add_argument("--prewarm-seconds", type=float, default=0.5,
+                    help="run steps for this long before the warmup steps, so the device clocks have ramped up")
     ap.add_argument("--cpu-single-seconds", type=float, default=3.0,
                     help="budget of the single-thread CPU oracle figure (0 skips it)")
     ap.add_argument("--schedule", default="auto", choices=["auto", "full", "symmetric", "full_64"],
@@ -178,10 +183,19 @@ def main() -> int:
     x = x_cpu.to(dev)
     sched = api.Schedule(cfg.B, cfg.N, cfg.D, dtype, cfg.insertions, schedule=args.schedule)
 
+    # Device pre-warm (outside the step count): the clocks of an idle device take a few
+    # hundred milliseconds of load to ramp up, longer than a handful of warmup steps.
+    prewarm_steps = 0
+    t_end = time.perf_counter() + args.prewarm_seconds
+    while time.perf_counter() < t_end:
+        for _ in range(8):
+            sched.run(x)
+        prewarm_steps += 8
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         sched.run(x)
     torch.cuda.synchronize()
-    log(f"bench: warmup {args.warmup} done, timing {args.steps} steps")
+    log(f"bench: pre-warm {prewarm_steps} steps, warmup {args.warmup} done, timing {args.steps} steps")
 
     # Timed region: K steps and nothing else on the stream between its two events.
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -304,8 +318,8 @@ def main() -> int:
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
     achieved = a_flops / len(a_idx) / (a_ms / len(a_idx) * 1e-3) / 1e12
     traffic = None
-    if TRAFFIC and TRAFFIC.get("source_sha256") == kernel_source_hash():
-        traffic = TRAFFIC["bytes_per_launch"]
+    if TRAFFIC.get("source_sha256") == kernel_source_hash() and args.schedule == "auto":
+        traffic = TRAFFIC["bytes_per_launch"].get(cfg.name)
     # The same launches counted by the matrix-core work they issue: below the
     # algorithmic figure under the symmetric schedule, which skips the blocks
     # below the diagonal.
@@ -332,6 +346,7 @@ def main() -> int:
                                 f"{cfg.insertions} MPM insertions + compose + gather"),
                    "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "none (1 GPU)"},
         "tokens_per_s": round(value * cfg.N, 0),
+        "prewarm": {"seconds": args.prewarm_seconds, "steps": prewarm_steps},
         "affinity_timed_steps": args.steps,
         "ms_per_step_with_per_kernel_events": round(ms_marked, 4),
         "survivors_mean": [round(sum(c) / len(c), 1) for c in counts],

@@ -46,7 +46,7 @@ def build_library(verbose: bool = False, extra_flags: list[str] | None = None) -
         out, _ = p.communicate()
         # hipcc's host pass does not know the packed-fp32 feature name; that note is harmless.
         lines = [ln for ln in out.splitlines() if "packed-fp32-ops" not in ln]
-        if lines and (verbose or p.returncode):
+        if lines and (verbose or p.returncode or any("warning" in ln for ln in lines)):
             print("\n".join(lines), flush=True)
         if p.returncode:
             failed.append(src)

@@ -596,8 +596,9 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         const uint32_t off = ioff.v[i];
         const uint32_t m0 =
             (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)(isb + (wave + WAVES * i) * RPI * CB);
-        asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0), "v"(off), "s"(ibase)
-                     : "memory", "m0");
+        // The LDS destination goes in M0, which the instruction reads implicitly: an input
+        // operand bound to M0, so the compiler sets it and knows the asm reads it.
+        asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(ibase), "{m0}"(m0) : "memory");
     };
     auto issue_end = [&]() {
         if (!iact) return;

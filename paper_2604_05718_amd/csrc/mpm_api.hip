@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
 
 #include <atomic>
 #include <mutex>
@@ -23,6 +25,26 @@ int hip_status(hipError_t e)
     g_last_hip_error = static_cast<int>(e);
     return MPM_ERR_HIP;
 }
+
+// Fault injection for testing callers' error paths without a GPU: with the
+// environment variable MPM_FAULT_INJECT=launch (read once, at the first call), every
+// entry point that would launch a kernel returns MPM_ERR_HIP with
+// hipErrorLaunchFailure recorded, after its argument checks and before any HIP call.
+bool inject_launch_failure()
+{
+    static const bool on = [] {
+        const char* v = getenv("MPM_FAULT_INJECT");
+        return v != nullptr && strcmp(v, "launch") == 0;
+    }();
+    return on;
+}
+
+int injected_failure() { return hip_status(hipErrorLaunchFailure); }
+
+#define MPM_LAUNCH_GATE()                                          \
+    do {                                                           \
+        if (inject_launch_failure()) return injected_failure();    \
+    } while (0)
 
 int check_shape(int32_t B, int32_t N)
 {
@@ -222,6 +244,7 @@ int mpm_workspace_init(void* ws, size_t ws_bytes, void* stream)
 {
     if (ws == nullptr || !aligned(ws, kAlign)) return MPM_ERR_INVALID_ARG;
     if (ws_bytes < kSyncWords * sizeof(int32_t)) return MPM_ERR_WORKSPACE;
+    MPM_LAUNCH_GATE();
     return hip_status(mpm::launch_zero_words(static_cast<int32_t*>(ws), (long)kSyncWords, as_stream(stream)));
 }
 
@@ -232,6 +255,7 @@ int mpm_affinity(const void* x, const int32_t* x_off, const float* x_inv, int32_
     if (s != MPM_OK) return s;
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
+    MPM_LAUNCH_GATE();
     return hip_status(mpm::launch_affinity(x, x_off, B, N, D, dt, schedule, w.pv, w.pi, as_stream(stream),
                                            static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event),
                                            x_inv));
@@ -246,6 +270,7 @@ int mpm_affinity_compact(const void* x, const int32_t* x_off, const float* x_inv
     if (!ok_int_ptr(map) || !ok_int_ptr(y_off)) return MPM_ERR_INVALID_ARG;
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
+    MPM_LAUNCH_GATE();
     return hip_status(affinity_compact(x, x_off, x_inv, B, N, D, dt, schedule, map, y_off, w,
                                        static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event),
                                        as_stream(stream)));
@@ -270,6 +295,7 @@ int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_
     if (!ok_int_ptr(nb) || !ok_opt_int_ptr(best)) return MPM_ERR_INVALID_ARG;
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
+    MPM_LAUNCH_GATE();
     const hipStream_t st = as_stream(stream);
     hipError_t e = mpm::launch_affinity(x, x_off, B, N, D, dt, schedule, w.pv, w.pi, st, nullptr, nullptr, nullptr);
     if (e == hipSuccess)
@@ -285,6 +311,7 @@ int mpm_pair_compact(const int32_t* nb, const int32_t* x_off, int32_t B, int32_t
     if (s != MPM_OK) return s;
     if (!ok_int_ptr(nb) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(map) || !ok_int_ptr(src) || !ok_int_ptr(y_off))
         return MPM_ERR_INVALID_ARG;
+    MPM_LAUNCH_GATE();
     return hip_status(mpm::launch_pair_compact(nb, x_off, B, N, map, src, y_off, nullptr, as_stream(stream)));
 }
 
@@ -296,6 +323,7 @@ int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, co
     if (!ok_rows_ptr(x) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(src) || !ok_int_ptr(y_off) || !ok_rows_ptr(y) ||
         !ok_opt_int_ptr(y_inv))
         return MPM_ERR_INVALID_ARG;
+    MPM_LAUNCH_GATE();
     return hip_status(mpm::launch_pair_average(x, x_off, src, y_off, B, N, D, dt, y, y_inv, as_stream(stream)));
 }
 
@@ -309,6 +337,7 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
         return MPM_ERR_INVALID_ARG;
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
+    MPM_LAUNCH_GATE();
     const hipStream_t st = as_stream(stream);
     hipError_t e = affinity_compact(x, x_off, x_inv, B, N, D, dt, schedule, map, y_off, w, nullptr, nullptr, st);
     if (e == hipSuccess) e = mpm::launch_pair_average(x, x_off, w.src, y_off, B, N, D, dt, y, y_inv, st);
@@ -323,6 +352,7 @@ int mpm_merge_noalloc(const void* x, const int32_t* x_off, const float* x_inv, i
     if (!ok_rows_ptr(y) || !ok_int_ptr(y_off) || !ok_opt_int_ptr(y_inv) || !ok_int_ptr(map))
         return MPM_ERR_INVALID_ARG;
     if (workspace_offsets(B, N).total > kScratchBytes) return MPM_ERR_WORKSPACE;
+    MPM_LAUNCH_GATE();
     const hipStream_t st = as_stream(stream);
     void* ws = nullptr;
     hipError_t e = scratch_for_current_device(st, &ws);
@@ -339,6 +369,7 @@ int mpm_compose(const int32_t* map_a, const int32_t* map_b, int32_t B, int32_t N
     const int s = check_shape(B, N);
     if (s != MPM_OK) return s;
     if (!ok_int_ptr(map_a) || !ok_int_ptr(map_b) || !ok_int_ptr(map_ab)) return MPM_ERR_INVALID_ARG;
+    MPM_LAUNCH_GATE();
     return hip_status(mpm::launch_compose(map_a, map_b, B, N, map_ab, as_stream(stream)));
 }
 
@@ -355,6 +386,7 @@ int mpm_compose_unmerge(const void* z, const int32_t* z_off, const int32_t* map_
         !ok_opt_int_ptr(map_ab) || !ok_rows_ptr(out))
         return MPM_ERR_INVALID_ARG;
     if (map_ab != nullptr && (map_ab == map_a || map_ab == map_b)) return MPM_ERR_INVALID_ARG;
+    MPM_LAUNCH_GATE();
     return hip_status(mpm::launch_unmerge(z, z_off, map_a, z_spec, E, B, N, D, dt, out, as_stream(stream), map_b,
                                           map_ab));
 }
@@ -368,6 +400,7 @@ int mpm_unmerge(const void* z, const int32_t* z_off, const int32_t* map, const v
         return MPM_ERR_INVALID_ARG;
     if ((long)E + N > MPM_MAX_N + (long)MPM_MAX_N) return MPM_ERR_UNSUPPORTED;
     if (!ok_rows_ptr(z) || !ok_opt_int_ptr(z_off) || !ok_int_ptr(map) || !ok_rows_ptr(out)) return MPM_ERR_INVALID_ARG;
+    MPM_LAUNCH_GATE();
     return hip_status(mpm::launch_unmerge(z, z_off, map, z_spec, E, B, N, D, dt, out, as_stream(stream)));
 }
 
