@@ -268,6 +268,31 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
               void* stream);
 
 /*
+ * One locality-constrained insertion: mpm_merge with the candidates of each token
+ * restricted to a window around it on the token grid, the mitigation of the
+ * quadratic affinity that the paper proposes (Sec. 5, also Sec. 4.3). A token's
+ * position is its raster index on a grid of grid_w columns (row = pos / grid_w,
+ * column = pos % grid_w):
+ *   pos (may be NULL): int32 per row of x, packed like x; NULL means each token's
+ *       index in its image (the raster order of a full grid, as for a first
+ *       insertion); positions must be non-decreasing in row along each image;
+ *   window >= 0: j is a candidate of i when |row_i - row_j| <= window and
+ *       |col_i - col_j| <= window;
+ *   nb[i] = argmax over the candidates of the cosine (lowest j on equal scores), or
+ *       -1 when the window holds no other token (i is then a singleton);
+ *   y_pos[y_off[b] + k] = the position of cluster k's representative (int32, packed
+ *       like y): the pos of the merged rows for the next insertion, which keeps the
+ *       raster order since ids follow the left-to-right scan.
+ * Only the candidate tiles a query block's window reaches are computed. The
+ * workspace as in mpm_merge (nb and src readable after the call). Errors as
+ * mpm_merge, plus MPM_ERR_INVALID_ARG for grid_w < 1, grid_w > MPM_MAX_N or
+ * window < 0. Positions outside [0, grid_w * MPM_MAX_N) are undefined behaviour.
+ */
+int mpm_merge_local(const void* x, const int32_t* x_off, const int32_t* pos, int32_t B, int32_t N, int32_t D,
+                    int32_t dt, int32_t grid_w, int32_t window, void* y, int32_t* y_off, int32_t* y_pos, int32_t* map,
+                    void* ws, size_t ws_bytes, void* stream);
+
+/*
  * mpm_merge for callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid allocation): the workspace
  * is a file-scope device array of MPM_NOALLOC_SCRATCH_BYTES that each GPU the

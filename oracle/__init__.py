@@ -14,6 +14,10 @@ chain the steps the way the paper does:
 * ``average``  -- cluster means (Eq. 2), rounded once to the storage dtype.
 * ``compose``  -- r*(i) = r2(r1(i)) (Eq. 3).
 * ``unmerge``  -- gather reconstruction Z_up[i] = Z[r*(i)] (Eq. 4).
+* the locality constraint of Sec. 5 (also Sec. 4.3): ``nearest``, ``merge`` and
+  ``schedule`` take token positions on the grid and a window radius; candidates
+  are restricted to the window, and a merged token takes its representative's
+  position.
 
 Parity status of each function is recorded in the tests: every function here is
 pinned by hand-derived cases and properties (see ``tests/test_oracle_*.py``).
@@ -46,6 +50,9 @@ def _load():
     lib = ctypes.CDLL(path)
     lib.mpm_oracle_nearest.argtypes = [_F64P, ctypes.c_int, ctypes.c_int, ctypes.c_int, _I32P, _F64P, _F64P]
     lib.mpm_oracle_nearest.restype = ctypes.c_int
+    lib.mpm_oracle_nearest_window.argtypes = [_F64P, ctypes.c_int, ctypes.c_int, _I32P, ctypes.c_int, ctypes.c_int,
+                                              ctypes.c_int, _I32P, _F64P, _F64P]
+    lib.mpm_oracle_nearest_window.restype = ctypes.c_int
     lib.mpm_oracle_nearest_from_affinity.argtypes = [_F64P, ctypes.c_int, _I32P]
     lib.mpm_oracle_nearest_from_affinity.restype = ctypes.c_int
     lib.mpm_oracle_pairs.argtypes = [_I32P, ctypes.c_int, _I32P, _I32P, _I32P]
@@ -106,8 +113,12 @@ class Nearest:
         return self.top1 - self.top2
 
 
-def nearest(x, threads: int | None = None) -> Nearest:
-    """b(i) = argmax_{j != i} cos(x_i, x_j), lowest j on equal values (Eq. 1, Sec. 3.2)."""
+def nearest(x, threads: int | None = None, pos=None, grid_w: int | None = None, window: int | None = None) -> Nearest:
+    """b(i) = argmax_{j != i} cos(x_i, x_j), lowest j on equal values (Eq. 1, Sec. 3.2).
+    With ``window`` (the locality constraint of Sec. 5): only tokens j whose grid
+    positions (``pos``: raster indices on a grid of ``grid_w`` columns; default the
+    raster order 0..n-1) lie within ``window`` rows and columns of token i's are
+    candidates; b(i) = -1 (top1 = top2 = -inf) when there is none."""
     lib = _load()
     x = _f64(x)
     n, D = x.shape
@@ -116,6 +127,14 @@ def nearest(x, threads: int | None = None) -> Nearest:
     nb = np.empty(n, np.int32)
     t1 = np.empty(n, np.float64)
     t2 = np.empty(n, np.float64)
+    if window is not None:
+        p = _i32(np.arange(n) if pos is None else pos)
+        rc = lib.mpm_oracle_nearest_window(_p(x, _F64P), n, D, _p(p, _I32P), int(grid_w), int(window),
+                                           threads or default_threads(), _p(nb, _I32P), _p(t1, _F64P),
+                                           _p(t2, _F64P))
+        if rc != 0:
+            raise RuntimeError("mpm_oracle_nearest_window failed")
+        return Nearest(nb, t1, t2)
     rc = lib.mpm_oracle_nearest(_p(x, _F64P), n, D, threads or default_threads(),
                                 _p(nb, _I32P), _p(t1, _F64P), _p(t2, _F64P))
     if rc != 0:
@@ -211,6 +230,7 @@ class MergeResult:
     nearest: Nearest
     pairs: Pairs
     y: np.ndarray       # float64 [n', D], values exactly representable in the storage dtype
+    y_pos: np.ndarray | None = None  # int32 [n']: grid position of each cluster (its representative's)
 
     @property
     def map(self) -> np.ndarray:
@@ -221,25 +241,39 @@ class MergeResult:
         return self.pairs.count
 
 
-def merge(x, dtype: str, threads: int | None = None, nb=None) -> MergeResult:
+def merge(x, dtype: str, threads: int | None = None, nb=None, pos=None, grid_w: int | None = None,
+          window: int | None = None) -> MergeResult:
     """One MPM call on one image (Alg. 1). ``nb`` replaces the nearest-neighbour
-    step (used to re-seed the later steps with another implementation's choice)."""
+    step (used to re-seed the later steps with another implementation's choice).
+    With ``window``: the locality-constrained neighbour of ``nearest``; the merged
+    tokens' positions are their representatives' (``y_pos``)."""
     x = _f64(x)
-    nn = nearest(x, threads) if nb is None else Nearest(_i32(nb), np.full(len(nb), np.nan), np.full(len(nb), np.nan))
+    if nb is not None:
+        nn = Nearest(_i32(nb), np.full(len(nb), np.nan), np.full(len(nb), np.nan))
+    else:
+        nn = nearest(x, threads, pos=pos, grid_w=grid_w, window=window)
     pr = pairs(nn.nb)
     y = average(x, pr.src_a, pr.src_b, dtype)
-    return MergeResult(nn, pr, y)
+    y_pos = None
+    if window is not None:
+        p = np.arange(x.shape[0], dtype=np.int32) if pos is None else _i32(pos)
+        y_pos = p[pr.src_a].copy()
+    return MergeResult(nn, pr, y, y_pos)
 
 
-def schedule(x, dtype: str, insertions: int = 2, threads: int | None = None):
+def schedule(x, dtype: str, insertions: int = 2, threads: int | None = None, grid_w: int | None = None,
+             window: int | None = None):
     """Insertions with identity blocks in between, then composition and
-    reconstruction (Sec. 3.3, Eq. 3, Eq. 4). Returns (stages, rstar, x_up)."""
+    reconstruction (Sec. 3.3, Eq. 3, Eq. 4). With ``window``, every insertion is
+    locality-constrained (Sec. 5) on a grid of ``grid_w`` columns, the first on the
+    raster positions. Returns (stages, rstar, x_up)."""
     cur = _f64(x)
     stages = []
     rstar = None
+    pos = None
     for _ in range(insertions):
-        res = merge(cur, dtype, threads)
+        res = merge(cur, dtype, threads, pos=pos, grid_w=grid_w, window=window)
         stages.append(res)
         rstar = res.map.copy() if rstar is None else compose(rstar, res.map)
-        cur = res.y
+        cur, pos = res.y, res.y_pos
     return stages, rstar, unmerge(cur, rstar)

@@ -16,7 +16,11 @@
  *   Eq. 2      : each cluster (one token or a mutual pair) is replaced by the
  *                mean of its members;
  *   Eq. 3      : composition of two merge maps, r*(i) = r2(r1(i));
- *   Eq. 4      : gather reconstruction, Z_up[i] = Z[r*(i)].
+ *   Eq. 4      : gather reconstruction, Z_up[i] = Z[r*(i)];
+ *   Sec. 5     : the locality constraint the paper proposes against the quadratic
+ *                affinity (also Sec. 4.3): candidates restricted to a spatial window
+ *                around each token (reading: Chebyshev radius on the token grid; a
+ *                merged token sits at its representative's position).
  *
  * Readings where the paper is silent:
  *   - ties in the argmax go to the lowest index j;
@@ -125,7 +129,20 @@ typedef struct {
     int32_t* nb;
     double* top1;
     double* top2;
+    const int32_t* pos;  /* NULL: every j != i is a candidate */
+    int grid_w, window;
 } nn_job;
+
+/* Whether token j is a candidate of token i under the locality constraint: both grid
+ * positions (raster indices on a grid of grid_w columns) within `window` rows and
+ * `window` columns of each other. */
+static int in_window(const nn_job* job, int i, int j)
+{
+    if (!job->pos) return 1;
+    const int ri = job->pos[i] / job->grid_w, ci = job->pos[i] % job->grid_w;
+    const int rj = job->pos[j] / job->grid_w, cj = job->pos[j] % job->grid_w;
+    return abs(ri - rj) <= job->window && abs(ci - cj) <= job->window;
+}
 
 /* For each row i: b(i) = argmax_{j != i} S_ij, lowest j among equal maxima;
  * top1 = the maximum, top2 = the second largest value over j != i (equal to
@@ -138,6 +155,7 @@ static void* nearest_rows(void* p)
         double v1 = -INFINITY, v2 = -INFINITY;
         for (int j = 0; j < job->n; ++j) {
             if (j == i) continue;  /* S_ii is -inf */
+            if (!in_window(job, i, j)) continue;  /* outside the locality window: not a candidate */
             double s = cosine_of(job->xt, job->D, i, j);
             if (best < 0 || s > v1) {
                 v2 = v1;
@@ -147,7 +165,7 @@ static void* nearest_rows(void* p)
                 v2 = s;
             }
         }
-        job->nb[i] = best;  /* -1 when the image has a single token */
+        job->nb[i] = best;  /* -1 when the image has a single token (or the window no other one) */
         if (job->top1) job->top1[i] = v1;
         if (job->top2) job->top2[i] = v2;
     }
@@ -157,8 +175,8 @@ static void* nearest_rows(void* p)
 /* x: n x D float64 (the storage values, converted exactly). Writes nb[n] and,
  * when non-NULL, top1[n] / top2[n]. Rows are split over `threads` threads.
  * Returns 0, or -1 on bad arguments / allocation failure. */
-int mpm_oracle_nearest(const double* x, int n, int D, int threads,
-                       int32_t* nb, double* top1, double* top2)
+static int nearest_impl(const double* x, int n, int D, int threads, int32_t* nb, double* top1, double* top2,
+                        const int32_t* pos, int grid_w, int window)
 {
     if (!x || !nb || n < 1 || D < 1) return -1;
     double* xt = (double*)malloc(sizeof(double) * (size_t)n * (size_t)D);
@@ -177,6 +195,7 @@ int mpm_oracle_nearest(const double* x, int n, int D, int threads,
         jobs[t].row_begin = (int)((int64_t)n * t / threads);
         jobs[t].row_end = (int)((int64_t)n * (t + 1) / threads);
         jobs[t].nb = nb; jobs[t].top1 = top1; jobs[t].top2 = top2;
+        jobs[t].pos = pos; jobs[t].grid_w = grid_w; jobs[t].window = window;
     }
     int spawned = 0;
     for (int t = 1; t < threads; ++t) {
@@ -188,6 +207,23 @@ int mpm_oracle_nearest(const double* x, int n, int D, int threads,
     for (int t = spawned + 1; t < threads; ++t) nearest_rows(&jobs[t]);  /* threads that failed to start */
     free(jobs); free(tids); free(xt);
     return 0;
+}
+
+int mpm_oracle_nearest(const double* x, int n, int D, int threads,
+                       int32_t* nb, double* top1, double* top2)
+{
+    return nearest_impl(x, n, D, threads, nb, top1, top2, NULL, 1, 0);
+}
+
+/* mpm_oracle_nearest under the locality constraint: pos[i] = grid position of token i
+ * (row * grid_w + col), window >= 0. Returns -1 on bad arguments. */
+int mpm_oracle_nearest_window(const double* x, int n, int D, const int32_t* pos, int grid_w, int window,
+                              int threads, int32_t* nb, double* top1, double* top2)
+{
+    if (!pos || grid_w < 1 || window < 0) return -1;
+    for (int i = 0; i < n; ++i)
+        if (pos[i] < 0) return -1;
+    return nearest_impl(x, n, D, threads, nb, top1, top2, pos, grid_w, window);
 }
 
 /* Same argmax rule applied to a given n x n matrix S (row-major); the diagonal

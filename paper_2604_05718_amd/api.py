@@ -165,6 +165,7 @@ class Merged:
     B: int
     N: int
     y_inv: torch.Tensor | None = None  # [B*N] float32 inverse norms of the rows of y, when asked for
+    y_pos: torch.Tensor | None = None  # [B*N] int32 grid positions of the rows of y (locality constraint)
 
     @property
     def nb(self) -> torch.Tensor:
@@ -218,6 +219,24 @@ def insertion(x, x_off=None, N=None, x_inv=None, want_inv=False, ws=None, schedu
     return Merged(y, y_off, m, ws, B, N, y_inv)
 
 
+def merge_local(x, grid_w: int, window: int, x_off=None, N=None, pos=None, ws=None) -> Merged:
+    """One locality-constrained insertion (Sec. 5): candidates within ``window`` rows and
+    columns on a grid of ``grid_w`` columns; ``pos`` the tokens' raster positions
+    (packed like x; None: each token's index in its image). The merged rows'
+    positions are returned in ``y_pos``."""
+    x2, B, N, D = _rows(x, N, x_off)
+    dev = x.device
+    ws = _workspace(B, N, dev, ws)
+    y = torch.empty((B * N, D), dtype=x.dtype, device=dev)
+    y_off = torch.empty((B + 1,), dtype=torch.int32, device=dev)
+    y_pos = torch.empty((B * N,), dtype=torch.int32, device=dev)
+    m = torch.empty((B, N), dtype=torch.int32, device=dev)
+    _lib.check("mpm_merge_local", _lib.load().mpm_merge_local(_p(x2), _p(x_off), _p(pos), B, N, D, _dt(x), int(grid_w),
+                                                              int(window), _p(y), _p(y_off), _p(y_pos), _p(m), _p(ws),
+                                                              ws.numel(), _stream()))
+    return Merged(y, y_off, m, ws, B, N, None, y_pos)
+
+
 def compose(map_a, map_b, out=None):
     """r*(i) = map_b[map_a[i]] per image (Eq. 3); maps [B, N] int32."""
     B, N = map_a.shape
@@ -268,22 +287,29 @@ class ScheduleResult:
     out: torch.Tensor     # reconstructed grid [B, N, D]
 
 
-def run_schedule(x, insertions: int = 2, workspaces=None, schedule: str = "auto") -> ScheduleResult:
+def run_schedule(x, insertions: int = 2, workspaces=None, schedule: str = "auto", grid_w: int | None = None,
+                 window: int | None = None) -> ScheduleResult:
     """Insertions with identity blocks in between (Sec. 3.3), composed maps
     (Eq. 3) and one gather back to the full grid (Eq. 4). Each insertion after the
     first takes the inverse norms of its input rows from the pair average that
-    wrote them (rows a whole number of 64 bytes), as Schedule does."""
+    wrote them (rows a whole number of 64 bytes), as Schedule does. With
+    ``window``, every insertion is locality-constrained (merge_local) on a grid of
+    ``grid_w`` columns, the first on the raster positions."""
     B, N, D = x.shape
-    norms = takes_norms(D, x.dtype)
+    norms = takes_norms(D, x.dtype) and window is None
     stages = []
-    cur, cur_off, cur_inv = x, None, None
+    cur, cur_off, cur_inv, cur_pos = x, None, None, None
     rstar = None
     for s in range(insertions):
         ws = None if workspaces is None else workspaces[s]
-        m = merge(cur, cur_off, N=N, x_inv=cur_inv, want_inv=norms and s + 1 < insertions, ws=ws, schedule=schedule)
+        if window is not None:
+            m = merge_local(cur, grid_w, window, x_off=cur_off, N=N, pos=cur_pos, ws=ws)
+        else:
+            m = merge(cur, cur_off, N=N, x_inv=cur_inv, want_inv=norms and s + 1 < insertions, ws=ws,
+                      schedule=schedule)
         stages.append(m)
         rstar = m.map if rstar is None else compose(rstar, m.map)
-        cur, cur_off, cur_inv = m.y, m.y_off, m.y_inv
+        cur, cur_off, cur_inv, cur_pos = m.y, m.y_off, m.y_inv, m.y_pos
     out = unmerge(cur, cur_off, rstar)
     return ScheduleResult(stages, rstar, out)
 
@@ -308,11 +334,12 @@ class Schedule:
     creates them lazily)."""
 
     def __init__(self, B: int, N: int, D: int, dtype: torch.dtype, insertions: int = 2, device="cuda",
-                 schedule: str = "auto"):
+                 schedule: str = "auto", grid_w: int | None = None, window: int | None = None):
         if insertions < 1:
             raise ValueError("at least one insertion")
         self.B, self.N, self.D, self.dtype, self.insertions = B, N, D, dtype, insertions
         self.schedule = _sched(schedule)
+        self.grid_w, self.window = grid_w, window  # locality constraint (merge_local) when window is set
         dev = torch.device(device)
         i32 = dict(dtype=torch.int32, device=dev)
         self.ws = [new_workspace(B, N, dev) for _ in range(insertions)]
@@ -322,9 +349,10 @@ class Schedule:
         self.y = [torch.empty((B * N, D), dtype=dtype, device=dev) for _ in range(insertions)]
         self.y_off = [torch.empty((B + 1,), **i32) for _ in range(insertions)]
         # Inverse norms of each insertion's merged rows, for the next insertion's affinity.
-        norms = takes_norms(D, dtype)
+        norms = takes_norms(D, dtype) and window is None
         self.y_inv = [torch.empty((B * N,), dtype=torch.float32, device=dev) if norms and s + 1 < insertions
                       else None for s in range(insertions)]
+        self.y_pos = [torch.empty((B * N,), **i32) if window is not None else None for _ in range(insertions)]
         # With one insertion the map is the composed map: the gather reads it directly.
         self.rstar = self.map[0] if insertions == 1 else torch.empty((B, N), **i32)
         self.rchain = torch.empty((B, N), **i32) if insertions > 2 else None  # maps composed before the last
@@ -336,7 +364,8 @@ class Schedule:
     def kernel_names(self) -> list:
         names = []
         for s in range(self.insertions):
-            names += [f"affinity+compact{s + 1}", f"average{s + 1}"]
+            names += [f"merge_local{s + 1}"] if self.window is not None else [f"affinity+compact{s + 1}",
+                                                                                 f"average{s + 1}"]
         if self.insertions == 1:
             return names + ["unmerge"]
         # the last composition runs inside the gather (mpm_compose_unmerge)
@@ -357,10 +386,16 @@ class Schedule:
                 marks[k].record()
             k += 1
 
-        cur, cur_off, cur_inv = x, None, None
+        cur, cur_off, cur_inv, cur_pos = x, None, None, None
         for s in range(self.insertions):
             ws = self.ws[s]
             mark()
+            if self.window is not None:
+                _lib.check("mpm_merge_local", lib.mpm_merge_local(
+                    _p(cur), _p(cur_off), _p(cur_pos), B, N, D, dt, self.grid_w, self.window, _p(self.y[s]),
+                    _p(self.y_off[s]), _p(self.y_pos[s]), _p(self.map[s]), _p(ws), ws.numel(), st))
+                cur, cur_off, cur_pos = self.y[s], self.y_off[s], self.y_pos[s]
+                continue
             ev0, ev1 = (None, None) if affinity_events is None else (c_event(e) for e in affinity_events[s])
             _lib.check("mpm_affinity_compact", lib.mpm_affinity_compact(
                 _p(cur), _p(cur_off), _p(cur_inv), B, N, D, dt, self.schedule, _p(self.map[s]), _p(self.y_off[s]),

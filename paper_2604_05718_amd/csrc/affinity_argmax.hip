@@ -95,10 +95,24 @@ __device__ __forceinline__ void lds_barrier()
 // workgroup owns QT queries and loops over every candidate tile itself.
 // WC x WQ waves; each wave computes MT x NT tiles of 32 candidates x 32 queries;
 // CHUNK bytes of the K dimension are staged per LDS buffer.
-template <class S, int WC, int WQ, int MT, int NT, int CHUNK>
+//
+// LOCAL: the locality constraint of Sec. 5 (candidates restricted to a window on the
+// token grid; positions in `win`). A token's position is a raster index on a grid of
+// win.grid_w columns (win.pos packed like x; null: the token's index in its image);
+// j is a candidate of i when both lie within win.radius rows and columns of each
+// other. Positions are non-decreasing in row along an image (raster order, which the
+// left-to-right ids keep for merged tokens), so the candidates of a query block lie in
+// a contiguous range of candidate tiles: only those are streamed, and every score is
+// masked by the window test.
+struct Window {
+    const int32_t* pos;
+    int grid_w, radius;
+};
+
+template <class S, int WC, int WQ, int MT, int NT, int CHUNK, bool LOCAL = false>
 __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int qblocks,
-    int xcd_major, int T, float* __restrict__ pv, int32_t* __restrict__ pi)
+    int xcd_major, int T, float* __restrict__ pv, int32_t* __restrict__ pi, Window win)
 {
     constexpr int THREADS = WC * WQ * kWave;
     constexpr int CT = WC * MT * 32;     // candidates per tile
@@ -114,6 +128,7 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
     __shared__ __attribute__((aligned(16))) float inv_c[2][CT];
     __shared__ float red_v[WC][QT];
     __shared__ int32_t red_i[WC][QT];
+    __shared__ int16_t cand_rc[LOCAL ? 2 : 1][LOCAL ? 2 * CT : 1];  // grid row and column per candidate
 
     // Workgroup -> (image, query block). With xcd_major, consecutive ids that the
     // hardware sends to the same XCD walk through the query blocks of one image
@@ -146,15 +161,24 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
     const uint8_t* ximg = x + (long)row0 * rowbytes;
     const int nchunks = (int)((rowbytes + CHUNK - 1) / CHUNK);
     const int ntiles = (n + CT - 1) / CT;
-    const int total = ntiles * nchunks;
+    // Candidate tiles [t_lo, t_hi] (all of them without the locality constraint).
+    int t_lo = 0, t_hi = ntiles - 1;
+    auto grid_pos = [&](int i) { return win.pos ? win.pos[row0 + i] : i; };
+    if (LOCAL) {
+        const int r_first = grid_pos(qbase) / win.grid_w;
+        const int r_last = grid_pos(min(qbase + QT, n) - 1) / win.grid_w;
+        while (t_lo < ntiles - 1 && grid_pos(min((t_lo + 1) * CT, n) - 1) / win.grid_w < r_first - win.radius) ++t_lo;
+        while (t_hi > t_lo && grid_pos(t_hi * CT) / win.grid_w > r_last + win.radius) --t_hi;
+    }
+    const int total = (t_hi - t_lo + 1) * nchunks;
 
     u32x4 pc[CLOADS];
     u32x4 pq[QLOADS];
     const u32x4 zero = {0u, 0u, 0u, 0u};
 
     auto gload = [&](int step) {
-        const int tile = step / nchunks;
-        const long kb = (long)(step - tile * nchunks) * CHUNK;
+        const int tile = t_lo + step / nchunks;
+        const long kb = (long)(step - (tile - t_lo) * nchunks) * CHUNK;
 #pragma unroll
         for (int u = 0; u < CLOADS; ++u) {
             const int slot = tid + u * THREADS;
@@ -230,9 +254,18 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
                 if (mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(a[mt], ss[mt]);
         }
 
-        const int tile = step / nchunks;
-        const bool tile_end = (step - tile * nchunks) == nchunks - 1;
+        const int tile = t_lo + step / nchunks;
+        const bool tile_end = (step - (tile - t_lo) * nchunks) == nchunks - 1;
         if (tile_end) {
+            if constexpr (LOCAL) {
+                // Grid row and column of each candidate of the tile (past the image: masked anyway).
+                for (int jl = tid; jl < CT; jl += THREADS) {
+                    const int j = tile * CT + jl;
+                    const int p = j < n ? grid_pos(j) : 0;
+                    cand_rc[tile & 1][2 * jl] = (int16_t)(p / win.grid_w);
+                    cand_rc[tile & 1][2 * jl + 1] = (int16_t)(p % win.grid_w);
+                }
+            }
             // Lanes l and l+32 hold the two k halves of candidate row lrow.
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
@@ -249,10 +282,16 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
             // Epilogue: scale by the candidate's inverse norm, mask, running argmax.
             const int cb = tile * CT;
             const float* iv = inv_c[tile & 1];
-            const bool need_mask = (cb + CT > n) || (cb < qbase + QT && qbase < cb + CT);
+            const bool need_mask = LOCAL || (cb + CT > n) || (cb < qbase + QT && qbase < cb + CT);
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) {
                 const int qi = qbase + wq * NT * 32 + nt * 32 + lrow;
+                int q_r = 0, q_c = 0;  // this lane's query cell (locality constraint)
+                if constexpr (LOCAL) {
+                    const int p = qi < n ? grid_pos(qi) : 0;
+                    q_r = p / win.grid_w;
+                    q_c = p % win.grid_w;
+                }
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
@@ -264,7 +303,13 @@ __global__ __launch_bounds__(WC * WQ * kWave) void affinity_argmax_kernel(
                         for (int e = 0; e < 4; ++e) {
                             const float s = acc[mt][nt][4 * g + e] * ivv[e];
                             const int j = cb + jl + e;
-                            const bool ok = !need_mask || (j < n && j != qi);
+                            bool ok = !need_mask || (j < n && j != qi);
+                            if constexpr (LOCAL) {
+                                const int dr = cand_rc[tile & 1][2 * (jl + e)] - q_r;
+                                const int dc = cand_rc[tile & 1][2 * (jl + e) + 1] - q_c;
+                                ok = ok && dr <= win.radius && -dr <= win.radius && dc <= win.radius &&
+                                     -dc <= win.radius;
+                            }
                             if (ok && s > bv[nt]) {
                                 bv[nt] = s;
                                 bi[nt] = j;
@@ -1065,17 +1110,17 @@ void launch_persistent(const void* x, const int32_t* x_off, const float* xinv, i
                               groups / xcds, pv, pi, xinv);
 }
 
-template <class S, int WC, int WQ, int MT, int NT, int CHUNK>
+template <class S, int WC, int WQ, int MT, int NT, int CHUNK, bool LOCAL = false>
 hipError_t launch_staged(const void* x, const int32_t* x_off, int B, int N, int D, int T, float* pv, int32_t* pi,
-                         hipStream_t stream, hipEvent_t start, hipEvent_t stop)
+                         hipStream_t stream, hipEvent_t start, hipEvent_t stop, Window win = Window{nullptr, 1, 0})
 {
     constexpr int QT = WQ * NT * 32;
     const int qblocks = (N + QT - 1) / QT;
     const int xcd_major = B >= kXcds ? 1 : 0;
     const long groups = xcd_major ? (long)kXcds * ((B + kXcds - 1) / kXcds) * qblocks : (long)B * qblocks;
-    hipExtLaunchKernelGGL((affinity_argmax_kernel<S, WC, WQ, MT, NT, CHUNK>), dim3((unsigned)groups),
+    hipExtLaunchKernelGGL((affinity_argmax_kernel<S, WC, WQ, MT, NT, CHUNK, LOCAL>), dim3((unsigned)groups),
                           dim3(WC * WQ * kWave), 0, stream, start, stop, 0, static_cast<const uint8_t*>(x), x_off, B, N,
-                          D, qblocks, xcd_major, T, pv, pi);
+                          D, qblocks, xcd_major, T, pv, pi, win);
     return hipGetLastError();
 }
 
@@ -1178,6 +1223,17 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
     }
     if (dt == kBf16) return launch_staged<Bf16, 2, 4, 4, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream, start, stop);
     return launch_staged<F32, 2, 2, 2, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream, start, stop);
+}
+
+hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const int32_t* pos, int grid_w, int radius,
+                                 int B, int N, int D, int dt, float* pv, int32_t* pi, hipStream_t stream,
+                                 hipEvent_t start, hipEvent_t stop)
+{
+    const int T = partial_tiles(N);
+    const Window win{pos, grid_w, radius};
+    if (dt == kBf16)
+        return launch_staged<Bf16, 2, 4, 2, 2, 128, true>(x, x_off, B, N, D, T, pv, pi, stream, start, stop, win);
+    return launch_staged<F32, 2, 2, 2, 2, 128, true>(x, x_off, B, N, D, T, pv, pi, stream, start, stop, win);
 }
 
 }  // namespace mpm

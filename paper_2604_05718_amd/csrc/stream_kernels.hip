@@ -113,7 +113,8 @@ __device__ __forceinline__ float vec_sumsq(u32x4 v, F32)
 template <class S>
 __global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, const int32_t* __restrict__ src,
-    const int32_t* __restrict__ y_off, int N, int D, int rows_per_block, uint8_t* __restrict__ y)
+    const int32_t* __restrict__ y_off, int N, int D, int rows_per_block, uint8_t* __restrict__ y,
+    const int32_t* __restrict__ pos, int32_t* __restrict__ y_pos)
 {
     const int b = blockIdx.y;
     const Span sp = output_span(y_off, b, N, gridDim.y);
@@ -136,6 +137,13 @@ __global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
             return out;
         },
         [&](long k, int c, u32x4 out) { store16(yimg + k * rowbytes + c * 16, out); });
+    if (y_pos) {  // grid positions of the merged rows (locality constraint): the representative's
+        const int32_t* posb = pos ? pos + (x_off ? x_off[b] : b * N) : nullptr;
+        for (int k = k0 + (int)threadIdx.x; k < k1; k += kRowThreads) {
+            const int rep = clamp_row(srcb[2 * k], nx);
+            y_pos[sp.off + k] = posb ? posb[rep] : rep;
+        }
+    }
 }
 
 // The pair average that also writes the inverse norm of every merged row, from the
@@ -265,14 +273,15 @@ int rows_per_block_for(long rowbytes, long block_bytes = kRowBytesPerBlock)
 }  // namespace
 
 hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* y_off, int B,
-                               int N, int D, int dt, void* y, float* y_inv, hipStream_t stream)
+                               int N, int D, int dt, void* y, float* y_inv, hipStream_t stream, const int32_t* pos,
+                               int32_t* y_pos)
 {
     const long rowbytes = (long)D * (dt == kBf16 ? 2 : 4);
     const int rpb = rows_per_block_for(rowbytes);
     dim3 grid((N + rpb - 1) / rpb, B);
     const uint8_t* xp = static_cast<const uint8_t*>(x);
     uint8_t* yp = static_cast<uint8_t*>(y);
-    if (y_inv) {
+    if (y_inv && !y_pos) {
         const int rows = kRowThreads / inv_lanes((int)(rowbytes / 16));
         const dim3 igrid((N + rows - 1) / rows, B);
         if (dt == kBf16)
@@ -285,10 +294,10 @@ hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_
     }
     if (dt == kBf16)
         hipLaunchKernelGGL(pair_average_kernel<Bf16>, grid, dim3(kRowThreads), 0, stream, xp, x_off, src, y_off, N, D,
-                           rpb, yp);
+                           rpb, yp, pos, y_pos);
     else
         hipLaunchKernelGGL(pair_average_kernel<F32>, grid, dim3(kRowThreads), 0, stream, xp, x_off, src, y_off, N, D,
-                           rpb, yp);
+                           rpb, yp, pos, y_pos);
     return hipGetLastError();
 }
 

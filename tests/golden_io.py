@@ -22,6 +22,8 @@ def load(name: str) -> dict:
                 rows.append([float(v) for v in val.split()])
             elif key == "clusters":
                 out[key] = [[int(v) for v in grp.split()] for grp in val.split("|")]
+            elif key in ("grid_w", "window"):
+                out[key] = int(val)
             elif key in ("layout", "stage1_rows", "stage2_rows"):
                 out[key] = val.split()
             elif key.startswith("block_") or key == "angles_deg":
@@ -46,3 +48,7 @@ def load(name: str) -> dict:
 
 def all_merge_cases():
     return sorted(f for f in os.listdir(GOLDEN) if f.startswith("h") and f.endswith(".txt"))
+
+
+def window_cases():
+    return sorted(f for f in os.listdir(GOLDEN) if f.startswith("w") and f.endswith(".txt"))

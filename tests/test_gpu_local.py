@@ -1,0 +1,129 @@
+"""Locality-constrained insertions (Sec. 5: the candidates of a token restricted to a
+window on the token grid) through mpm_merge_local, against the oracle with the same
+window: the hand-derived grid, random grids of several sizes, windows and ragged
+second insertions (positions carried by the merged rows), and the ViT-B and ViT-L
+token grids at full batch size, stage by stage with the near-tie rule."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2604_05718_amd as mpm
+from golden_io import load
+from paper_2604_05718_amd import synth
+from parity import check_nearest, rel_err, to64, FEATURE_RTOL
+
+pytestmark = pytest.mark.gpu
+
+DEV = torch.device("cuda:0")
+TORCH_DT = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def store(x64, dtype):
+    return torch.from_numpy(np.asarray(x64, np.float32)).to(TORCH_DT[dtype])
+
+
+def check_local_schedule_image(x_img, dtype, res, b, grid_w, window, threads=None):
+    """Stage by stage: the GPU's neighbours against the oracle's windowed ones (near-tie
+    rule), then maps, merged rows and positions against the oracle seeded with them;
+    end to end against the oracle's windowed schedule when nothing flipped."""
+    cur = to64(x_img)
+    pos = np.arange(cur.shape[0], dtype=np.int32)
+    flips, maps = 0, []
+    for s, st in enumerate(res.stages):
+        n = cur.shape[0]
+        nb = st.nb[b].cpu().numpy()[:n]
+        # Neighbours: -1 exactly where the window holds no other token.
+        nn = oracle.nearest(cur, threads, pos=pos, grid_w=grid_w, window=window)
+        empty = nn.nb < 0
+        assert np.array_equal(nb[empty], nn.nb[empty]) and np.all(nb[~empty] >= 0), f"stage {s + 1}: empty windows"
+        idx = np.flatnonzero(~empty)
+        if idx.size:
+            # the near-tie check on rows with candidates: compare against the windowed top-1/2
+            gap = nn.top1 - nn.top2
+            for i in idx[nb[idx] != nn.nb[idx]]:
+                j = int(nb[i])
+                pi, pj = pos[i], pos[j]
+                inside = abs(pi // grid_w - pj // grid_w) <= window and abs(pi % grid_w - pj % grid_w) <= window
+                sc = oracle.cosine(cur, int(i), j)
+                assert inside and gap[i] < 1e-5 and sc >= nn.top1[i] - 1e-5, f"stage {s + 1} row {i}"
+                flips += 1
+        ref = oracle.merge(cur, dtype, nb=nb, pos=pos, grid_w=grid_w, window=window)
+        m = st.map[b].cpu().numpy()
+        assert np.array_equal(m[:n], ref.map) and np.all(m[n:] == -1), f"stage {s + 1}: map"
+        off = st.y_off.cpu().numpy()
+        y = to64(st.y[off[b]:off[b + 1]])
+        assert y.shape[0] == ref.count
+        assert rel_err(y, ref.y) <= FEATURE_RTOL[dtype]
+        yp = st.y_pos[off[b]:off[b + 1]].cpu().numpy()
+        assert np.array_equal(yp, ref.y_pos), f"stage {s + 1}: positions"
+        maps.append(m[:n])
+        cur, pos = y, yp
+    rstar = maps[0]
+    for m in maps[1:]:
+        rstar = oracle.compose(rstar, m)
+    assert np.array_equal(res.rstar[b].cpu().numpy(), rstar)
+    assert np.array_equal(to64(res.out[b]), oracle.unmerge(cur, rstar))
+    if flips == 0:
+        stages, r_ref, up_ref = oracle.schedule(to64(x_img), dtype, insertions=len(res.stages), threads=threads,
+                                                grid_w=grid_w, window=window)
+        assert np.array_equal(res.rstar[b].cpu().numpy(), r_ref), "end-to-end composed map"
+    return flips
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_window_hand_case_on_gpu(dtype):
+    g = load("w1_window.txt")
+    x = np.zeros((9, 16))
+    x[:, :2] = g["x"]
+    xt = store(oracle.round_to(x, dtype), dtype)[None].to(DEV)
+    res = mpm.merge_local(xt, g["grid_w"], g["window"])
+    torch.cuda.synchronize()
+    assert res.nb[0].cpu().tolist() == g["nb"]
+    assert res.map[0].cpu().tolist() == g["map"]
+    assert res.y_off.cpu().tolist() == [0, g["count"]]
+    assert res.y_pos[: g["count"]].cpu().tolist() == g["y_pos"]
+
+
+CASES = [  # (grid rows, grid cols, D, window, images)
+    (5, 7, 64, 1, 3), (16, 16, 128, 2, 4), (17, 31, 96, 3, 2), (32, 32, 192, 0, 2), (20, 24, 64, 30, 2),
+    (40, 40, 256, 4, 3)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("gh,gw,D,window,B", CASES)
+def test_local_schedule_random_grids(dtype, gh, gw, D, window, B):
+    """Two windowed insertions on clustered tokens (the second on the ragged packed
+    survivors and their carried positions), composition and gather, every image
+    checked; window 0 leaves every token alone, a window covering the grid is the
+    dense method."""
+    rng = np.random.default_rng(gh * 1000 + gw * 10 + window)
+    N = gh * gw
+    imgs = []
+    for _ in range(B):
+        cent = rng.standard_normal((12, D))
+        lab = rng.integers(0, 12, N)
+        imgs.append(store(cent[lab] + 0.3 * rng.standard_normal((N, D)), dtype))
+    x = torch.stack(imgs)
+    print(f"local schedule {dtype} grid {gh}x{gw} D={D} window={window} B={B}", flush=True)
+    res = mpm.run_schedule(x.to(DEV), insertions=2, grid_w=gw, window=window)
+    torch.cuda.synchronize()
+    for b in range(B):
+        check_local_schedule_image(x[b], dtype, res, b, gw, window)
+    if window == 0:
+        assert res.stages[0].y_off.cpu().tolist() == [N * k for k in range(B + 1)]
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,window,images", [("vit_b_512", 3, [0, 21, 63]), ("vit_l_1024", 4, [0, 9, 15])])
+def test_local_schedule_full_size(name, window, images):
+    """The windowed schedule on a full benchmark batch (the launch configuration
+    bench.py --window times), sampled images checked completely."""
+    cfg = synth.config(name)
+    x = synth.make_batch(cfg, seed=0)
+    print(f"local schedule {name} window={window}: B={cfg.B} N={cfg.N} D={cfg.D}", flush=True)
+    res = mpm.run_schedule(x.to(DEV), insertions=cfg.insertions, grid_w=cfg.G, window=window)
+    torch.cuda.synchronize()
+    flips = sum(check_local_schedule_image(x[b], cfg.dtype, res, b, cfg.G, window) for b in images)
+    counts = [torch.diff(st.y_off.cpu()).tolist() for st in res.stages]
+    print(f"  survivors (mean): {[round(sum(c) / len(c), 1) for c in counts]}, accepted flips {flips}", flush=True)

@@ -134,3 +134,22 @@ def test_top1_top2_hand_derived():
     assert np.all(np.isneginf(nn.top2))
     nn = oracle.nearest(_unit([30.0]))  # one token: no candidate at all
     assert nn.nb[0] == -1 and np.isneginf(nn.top1[0]) and np.isneginf(nn.top2[0])
+
+
+def test_window_hand_case():
+    """The locality-constrained neighbour (Sec. 5) on a hand-derived 3x3 grid: every
+    neighbour, pair, id, cluster and merged position, and the dense choice the window
+    rules out."""
+    g = load("w1_window.txt")
+    x = g["x"]
+    for dtype in ("f32", "bf16"):
+        xs = oracle.round_to(x, dtype)
+        res = oracle.merge(xs, dtype, grid_w=g["grid_w"], window=g["window"])
+        assert res.nearest.nb.tolist() == g["nb"]
+        assert res.map.tolist() == g["map"]
+        assert res.count == g["count"]
+        assert res.y_pos.tolist() == g["y_pos"]
+        for k, members in enumerate(g["clusters"]):
+            np.testing.assert_array_equal(res.y[k], oracle.round_to(xs[members].mean(axis=0), dtype))
+    dense = oracle.nearest(x)
+    assert dense.nb[0] == g["dense_nb0"] and dense.nb[8] == g["dense_nb8"]

@@ -245,3 +245,83 @@ def test_round_to_hand_ties():
     # float32: C conversion rounds to nearest even.
     assert oracle.round_to(np.array([1 + 2**-24]), "f32")[0] == 1.0
     assert oracle.round_to(np.array([1 + 3 * 2**-24]), "f32")[0] == 1 + 2**-22
+
+
+# ---- the locality constraint (Sec. 5) ---------------------------------------------------
+
+def _grid_tokens(rng, gh, gw, D, k=4):
+    cent = rng.standard_normal((k, D))
+    lab = rng.integers(0, k, gh * gw)
+    return cent[lab] + 0.3 * rng.standard_normal((gh * gw, D))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_window_covering_the_grid_is_the_dense_definition(seed):
+    """A window at least as wide as the grid admits every other token: exactly the
+    dense oracle (neighbours and both top values)."""
+    rng = np.random.default_rng(seed)
+    gh, gw = int(rng.integers(1, 7)), int(rng.integers(1, 7))
+    x = _grid_tokens(rng, gh, gw, 5)
+    dense = oracle.nearest(x)
+    win = oracle.nearest(x, grid_w=gw, window=max(gh, gw) - 1 + int(rng.integers(0, 3)))
+    assert np.array_equal(win.nb, dense.nb)
+    assert np.array_equal(win.top1, dense.top1) and np.array_equal(win.top2, dense.top2)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_window_zero_leaves_every_token_alone(dtype):
+    """Radius 0 admits no other token: every token is a singleton, the merge is the
+    identity (N' = N, r(i) = i, rows copied), positions unchanged."""
+    rng = np.random.default_rng(7)
+    x = oracle.round_to(_grid_tokens(rng, 5, 6, 8), dtype)
+    res = oracle.merge(x, dtype, grid_w=6, window=0)
+    assert np.all(res.nearest.nb == -1) and np.all(np.isneginf(res.nearest.top1))
+    assert res.count == 30 and res.map.tolist() == list(range(30))
+    assert np.array_equal(res.y, x) and res.y_pos.tolist() == list(range(30))
+
+
+@settings(max_examples=200, deadline=None)
+@given(seed=st.integers(0, 2**31 - 1), gh=st.integers(1, 6), gw=st.integers(1, 6), window=st.integers(0, 3),
+       D=st.integers(1, 6))
+def test_window_choice_is_the_best_inside_the_window(seed, gh, gw, window, D):
+    """Every windowed neighbour lies inside the window and attains the largest cosine
+    there (lowest index among equals); a row whose dense neighbour lies inside the
+    window keeps it; the window never raises a row's best score."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((gh * gw, D)).round(1)  # rounding makes exact ties common
+    n = gh * gw
+    win = oracle.nearest(x, grid_w=gw, window=window)
+    dense = oracle.nearest(x)
+    for i in range(n):
+        cand = [j for j in range(n) if j != i and abs(j // gw - i // gw) <= window and abs(j % gw - i % gw) <= window]
+        if not cand:
+            assert win.nb[i] == -1
+            continue
+        s = np.array([oracle.cosine(x, i, j) for j in cand])
+        assert win.nb[i] == cand[int(np.flatnonzero(s == s.max())[0])]
+        assert win.top1[i] == s.max() <= dense.top1[i]
+        if dense.nb[i] in cand:
+            assert win.nb[i] == dense.nb[i]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_window_schedule_positions(seed):
+    """Over two insertions the merged tokens keep their representatives' cells: each
+    stage's positions are a strictly increasing (raster-order) subset of the
+    previous stage's, and every cluster's members lie within the window of its
+    representative; the pairing invariants hold (except N' <= N - 1: a window may
+    leave a token without candidates)."""
+    rng = np.random.default_rng(100 + seed)
+    gh, gw, window = 6, 7, int(rng.integers(1, 3))
+    x = _grid_tokens(rng, gh, gw, 6)
+    stages, rstar, up = oracle.schedule(x, "f32", insertions=2, grid_w=gw, window=window)
+    pos = np.arange(gh * gw)
+    for stg in stages:
+        assert np.all(np.diff(stg.y_pos) > 0) and set(stg.y_pos.tolist()) <= set(pos.tolist())
+        for a, b in zip(stg.pairs.src_a, stg.pairs.src_b):
+            pa, pb = pos[a], pos[b]
+            assert abs(pa // gw - pb // gw) <= window and abs(pa % gw - pb % gw) <= window
+        n = pos.shape[0]
+        assert (n + 1) // 2 <= stg.count <= n
+        pos = stg.y_pos
+    assert np.array_equal(up, oracle.unmerge(stages[-1].y, rstar))
