@@ -95,6 +95,33 @@ def algorithmic_work(cfg, counts):
     return work
 
 
+def window_candidates(positions, grid: int, window: int) -> int:
+    """Sum over tokens of the number of other tokens inside their window (the locality
+    constraint): positions = raster indices of one image's tokens on a grid x grid grid."""
+    import numpy as np
+
+    occ = np.zeros((grid, grid), np.int64)
+    occ.flat[np.asarray(positions)] = 1
+    cs = np.zeros((grid + 1, grid + 1), np.int64)
+    cs[1:, 1:] = occ.cumsum(0).cumsum(1)
+    r, c = np.divmod(np.asarray(positions), grid)
+    r0, r1 = np.clip(r - window, 0, grid), np.clip(r + window + 1, 0, grid)
+    c0, c1 = np.clip(c - window, 0, grid), np.clip(c + window + 1, 0, grid)
+    inside = cs[r1, c1] - cs[r0, c1] - cs[r1, c0] + cs[r0, c0]
+    return int((inside - 1).sum())
+
+
+def algorithmic_work_local(cfg, counts, stage_positions, window):
+    """algorithmic_work for locality-constrained insertions: each insertion's affinity
+    costs 2 D flops per (token, candidate in its window) pair; the merge_local step
+    also holds the compaction and the pair average."""
+    work = []
+    for st in range(cfg.insertions):
+        work.append(("flops", sum(2.0 * cfg.D * window_candidates(p, cfg.G, window) for p in stage_positions[st])))
+    dense = algorithmic_work(cfg, counts)
+    return work + dense[2 * cfg.insertions:]
+
+
 def cpu_baseline(cfg, x_cpu, budget_s: float, threads: int | None = None):
     import oracle
 
@@ -148,6 +175,8 @@ def main() -> int:
                     help="budget of the single-thread CPU oracle figure (0 skips it)")
     ap.add_argument("--schedule", default="auto", choices=["auto", "full", "symmetric", "full_64"],
                     help="affinity work schedule (auto: the library's choice for the batch shape)")
+    ap.add_argument("--window", type=int, default=None,
+                    help="locality-constrained merging (Sec. 5): candidates within this many grid rows and columns")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run 5 device-to-device copies of this many MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -181,7 +210,8 @@ def main() -> int:
     log(f"bench: {cfg.name} B={cfg.B} N={cfg.N} D={cfg.D} {cfg.dtype}, generating inputs")
     x_cpu = synth.make_batch(cfg, seed=0)
     x = x_cpu.to(dev)
-    sched = api.Schedule(cfg.B, cfg.N, cfg.D, dtype, cfg.insertions, schedule=args.schedule)
+    sched = api.Schedule(cfg.B, cfg.N, cfg.D, dtype, cfg.insertions, schedule=args.schedule,
+                         grid_w=cfg.G if args.window is not None else None, window=args.window)
 
     # Device pre-warm (outside the step count): the clocks of an idle device take a few
     # hundred milliseconds of load to ramp up, longer than a handful of warmup steps.
@@ -239,7 +269,15 @@ def main() -> int:
     names = sched.kernel_names
     per_kernel_ms = [sum(m[i].elapsed_time(m[i + 1]) for m in marks) / args.steps for i in range(len(names))]
     counts = [torch.diff(sched.y_off[s].cpu()).tolist() for s in range(cfg.insertions)]
-    work = algorithmic_work(cfg, counts)
+    if args.window is None:
+        work = algorithmic_work(cfg, counts)
+    else:
+        stage_positions = [[list(range(cfg.N))] * cfg.B]
+        for s in range(cfg.insertions - 1):
+            off = sched.y_off[s].cpu().tolist()
+            yp = sched.y_pos[s].cpu()
+            stage_positions.append([yp[off[b]:off[b + 1]].tolist() for b in range(cfg.B)])
+        work = algorithmic_work_local(cfg, counts, stage_positions, args.window)
 
     # Step-time distribution: one event per step boundary (outside the timed region).
     bounds = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
@@ -297,36 +335,41 @@ def main() -> int:
         graph = {"error": f"{type(exc).__name__}: {exc}"}
 
     schedule = mpm.affinity_schedule_used(cfg.B, cfg.N, cfg.D, dtype, args.schedule)
-    executed = executed_affinity_flops(cfg, counts, schedule)
+    if args.window is not None:
+        schedule = f"window {args.window}"
+    executed = executed_affinity_flops(cfg, counts, schedule) if args.window is None else None
     kernels = []
     for name, ms, (kind, amount) in zip(names, per_kernel_ms, work):
         ent = {"name": name, "us": round(ms * 1e3, 2)}
         if kind == "flops":
             tf = amount / (ms * 1e-3) / 1e12
             peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
-            ent.update({"gflop": round(amount / 1e9, 3), "tflops": round(tf, 1), "frac_mfma": round(tf / peak, 4),
-                        "executed_gflop": round(executed[int(name[len("affinity+compact"):]) - 1] / 1e9, 3)})
+            ent.update({"gflop": round(amount / 1e9, 3), "tflops": round(tf, 1), "frac_mfma": round(tf / peak, 4)})
+            if executed is not None:
+                ent["executed_gflop"] = round(executed[int(name[len("affinity+compact"):]) - 1] / 1e9, 3)
         else:
             gbs = amount / (ms * 1e-3) / 1e9
             ent.update({"mbytes": round(amount / 1e6, 3), "gbs": round(gbs, 1), "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
         kernels.append(ent)
 
     # Dominant kernel: the fused affinity-argmax (both insertions' launches).
-    a_idx = [i for i, n in enumerate(names) if n.startswith("affinity")]
+    a_idx = [i for i, n in enumerate(names) if n.startswith("affinity") or n.startswith("merge_local")]
     a_flops = sum(work[i][1] for i in a_idx)
     a_ms = sum(aff_ms)
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
     achieved = a_flops / len(a_idx) / (a_ms / len(a_idx) * 1e-3) / 1e12
     traffic = None
-    if TRAFFIC.get("source_sha256") == kernel_source_hash() and args.schedule == "auto":
+    if (TRAFFIC.get("source_sha256") == kernel_source_hash() and args.schedule == "auto" and
+            args.window is None):
         traffic = TRAFFIC["bytes_per_launch"].get(cfg.name)
-    # The same launches counted by the matrix-core work they issue: below the
-    # algorithmic figure under the symmetric schedule, which skips the blocks
-    # below the diagonal.
-    issued = sum(executed) / len(a_idx) / (a_ms / len(a_idx) * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": traffic, "schedule": schedule,
-                "issued": round(issued, 1), "frac_issued": round(issued / peak, 4)}
+                "frac": round(achieved / peak, 4), "traffic": traffic, "schedule": schedule}
+    if executed is not None:
+        # The same launches counted by the matrix-core work they issue: below the
+        # algorithmic figure under the symmetric schedule, which skips the blocks
+        # below the diagonal.
+        issued = sum(executed) / len(a_idx) / (a_ms / len(a_idx) * 1e-3) / 1e12
+        roofline.update({"issued": round(issued, 1), "frac_issued": round(issued / peak, 4)})
 
     value = cfg.B / (ms_per_step * 1e-3)
     result = {
@@ -343,7 +386,9 @@ def main() -> int:
         "dtype": cfg.dtype,
         "data": "synthetic",
         "config": {"workload": (f"{cfg.name}: ViT token grid {cfg.G}x{cfg.G} (N={cfg.N}), D={cfg.D}, B={cfg.B}, "
-                                f"{cfg.insertions} MPM insertions + compose + gather"),
+                                f"{cfg.insertions} MPM insertions + compose + gather"
+                                + ("" if args.window is None else
+                                   f", locality-constrained (window {args.window})")),
                    "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "none (1 GPU)"},
         "tokens_per_s": round(value * cfg.N, 0),
         "prewarm": {"seconds": args.prewarm_seconds, "steps": prewarm_steps},

@@ -284,13 +284,15 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
  *       like y): the pos of the merged rows for the next insertion, which keeps the
  *       raster order since ids follow the left-to-right scan.
  * Only the candidate tiles a query block's window reaches are computed. The
- * workspace as in mpm_merge (nb and src readable after the call). Errors as
+ * workspace as in mpm_merge (nb and src readable after the call). start_event /
+ * stop_event (may be NULL) are bound to the affinity kernel's dispatch, as in
+ * mpm_affinity. Errors as
  * mpm_merge, plus MPM_ERR_INVALID_ARG for grid_w < 1, grid_w > MPM_MAX_N or
  * window < 0. Positions outside [0, grid_w * MPM_MAX_N) are undefined behaviour.
  */
 int mpm_merge_local(const void* x, const int32_t* x_off, const int32_t* pos, int32_t B, int32_t N, int32_t D,
                     int32_t dt, int32_t grid_w, int32_t window, void* y, int32_t* y_off, int32_t* y_pos, int32_t* map,
-                    void* ws, size_t ws_bytes, void* stream);
+                    void* ws, size_t ws_bytes, void* start_event, void* stop_event, void* stream);
 
 /*
  * mpm_merge for callers that cannot allocate device memory (code under HIP graph

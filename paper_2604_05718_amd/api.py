@@ -233,7 +233,7 @@ def merge_local(x, grid_w: int, window: int, x_off=None, N=None, pos=None, ws=No
     m = torch.empty((B, N), dtype=torch.int32, device=dev)
     _lib.check("mpm_merge_local", _lib.load().mpm_merge_local(_p(x2), _p(x_off), _p(pos), B, N, D, _dt(x), int(grid_w),
                                                               int(window), _p(y), _p(y_off), _p(y_pos), _p(m), _p(ws),
-                                                              ws.numel(), _stream()))
+                                                              ws.numel(), None, None, _stream()))
     return Merged(y, y_off, m, ws, B, N, None, y_pos)
 
 
@@ -391,9 +391,10 @@ class Schedule:
             ws = self.ws[s]
             mark()
             if self.window is not None:
+                ev0, ev1 = (None, None) if affinity_events is None else (c_event(e) for e in affinity_events[s])
                 _lib.check("mpm_merge_local", lib.mpm_merge_local(
                     _p(cur), _p(cur_off), _p(cur_pos), B, N, D, dt, self.grid_w, self.window, _p(self.y[s]),
-                    _p(self.y_off[s]), _p(self.y_pos[s]), _p(self.map[s]), _p(ws), ws.numel(), st))
+                    _p(self.y_off[s]), _p(self.y_pos[s]), _p(self.map[s]), _p(ws), ws.numel(), ev0, ev1, st))
                 cur, cur_off, cur_pos = self.y[s], self.y_off[s], self.y_pos[s]
                 continue
             ev0, ev1 = (None, None) if affinity_events is None else (c_event(e) for e in affinity_events[s])

@@ -366,7 +366,7 @@ int mpm_merge_noalloc(const void* x, const int32_t* x_off, const float* x_inv, i
 
 int mpm_merge_local(const void* x, const int32_t* x_off, const int32_t* pos, int32_t B, int32_t N, int32_t D,
                     int32_t dt, int32_t grid_w, int32_t window, void* y, int32_t* y_off, int32_t* y_pos, int32_t* map,
-                    void* ws, size_t ws_bytes, void* stream)
+                    void* ws, size_t ws_bytes, void* start_event, void* stop_event, void* stream)
 {
     int s = check_affinity(x, x_off, nullptr, B, N, D, dt, MPM_SCHEDULE_AUTO);
     if (s != MPM_OK) return s;
@@ -378,8 +378,9 @@ int mpm_merge_local(const void* x, const int32_t* x_off, const int32_t* pos, int
     MPM_LAUNCH_GATE();
     const hipStream_t st = as_stream(stream);
     // One partial per token (the kernel covers every candidate tile of the window itself).
-    hipError_t e = mpm::launch_affinity_local(x, x_off, pos, grid_w, window, B, N, D, dt, w.pv, w.pi, st, nullptr,
-                                              nullptr);
+    hipError_t e = mpm::launch_affinity_local(x, x_off, pos, grid_w, window, B, N, D, dt, w.pv, w.pi, st,
+                                              static_cast<hipEvent_t>(start_event),
+                                              static_cast<hipEvent_t>(stop_event));
     if (e == hipSuccess)
         e = mpm::launch_pair_compact_partials(w.pv, w.pi, mpm::partial_tiles(N), N, w.nb, x_off, B, N, map, w.src,
                                               y_off, w.sync, st);
