@@ -149,6 +149,59 @@ def cpu_baseline(cfg, x_cpu, budget_s: float, threads: int | None = None):
     }
 
 
+def backbone(args, cfg, dev) -> int:
+    """The paper's end-to-end setting on this build: a ViT encoder (random weights, 12
+    blocks, the workload's width, 64-wide heads) with MPM before blocks 2 and 5 and the
+    gather after the last block, against the same encoder without merging; whole
+    forward passes timed, images/s for both."""
+    import torch
+
+    from paper_2604_05718_amd import synth
+    from paper_2604_05718_amd.encoder import Encoder
+
+    dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    x = synth.make_batch(cfg, seed=0).to(dev)
+    heads = cfg.D // 64
+    res = {}
+    for name, merge_before, attn in (("plain", (), "varlen"), ("mpm_2_5", (2, 5), "varlen"),
+                                     ("plain_padded_attention", (), "padded"),
+                                     ("mpm_2_5_padded_attention", (2, 5), "padded")):
+        enc = Encoder(D=cfg.D, heads=heads, depth=12, merge_before=merge_before, dtype=dtype, device=dev,
+                      attn=attn)
+        for _ in range(max(2, args.warmup)):
+            enc.forward(x)
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(args.steps):
+            enc.forward(x)
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / args.steps
+        res[name] = {"ms_per_forward": round(ms, 3), "images_per_s": round(cfg.B / (ms * 1e-3), 1)}
+        if merge_before:
+            res[name]["tokens_after_each_merge_mean"] = [round(sum(c) / len(c), 1) for c in enc.last_counts]
+        log(f"bench: backbone {name}: {ms:.2f} ms per forward")
+        del enc
+        torch.cuda.empty_cache()
+    out = {
+        "metric": f"ViT encoder forward images/s, MPM before blocks 2 and 5 vs none ({cfg.name} tokens)",
+        "value": res["mpm_2_5"]["images_per_s"], "unit": "images/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": res["mpm_2_5"]["ms_per_forward"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic tokens, random weights",
+        "config": {"workload": f"{cfg.name}: 12-block ViT encoder, D={cfg.D}, {heads} heads, B={cfg.B}, N={cfg.N}",
+                   "global_batch": cfg.B, "seq_len": cfg.N, "parallelism": "none (1 GPU)"},
+        "attention": "torch variable-length flash attention on the packed rows",
+        "plain": res["plain"], "mpm": res["mpm_2_5"],
+        "speedup": round(res["plain"]["ms_per_forward"] / res["mpm_2_5"]["ms_per_forward"], 4),
+        "padded_attention": {"plain": res["plain_padded_attention"], "mpm": res["mpm_2_5_padded_attention"],
+                             "speedup": round(res["plain_padded_attention"]["ms_per_forward"] /
+                                              res["mpm_2_5_padded_attention"]["ms_per_forward"], 4)},
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -177,6 +230,9 @@ def main() -> int:
                     help="affinity work schedule (auto: the library's choice for the batch shape)")
     ap.add_argument("--window", type=int, default=None,
                     help="locality-constrained merging (Sec. 5): candidates within this many grid rows and columns")
+    ap.add_argument("--backbone", action="store_true",
+                    help="time a random-weight ViT encoder of the workload's width with MPM before blocks 2 and 5 "
+                         "against the plain encoder, and print that instead")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run 5 device-to-device copies of this many MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -206,6 +262,8 @@ def main() -> int:
 
     cfg = synth.config(args.workload)
     dev = torch.device("cuda:0")
+    if args.backbone:
+        return backbone(args, cfg, dev)
     dtype = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     log(f"bench: {cfg.name} B={cfg.B} N={cfg.N} D={cfg.D} {cfg.dtype}, generating inputs")
     x_cpu = synth.make_batch(cfg, seed=0)

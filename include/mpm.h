@@ -295,6 +295,26 @@ int mpm_merge_local(const void* x, const int32_t* x_off, const int32_t* pos, int
                     void* ws, size_t ws_bytes, void* start_event, void* stop_event, void* stream);
 
 /*
+ * Padded batch layout (the paper pads each batch to its longest image, Sec. 4.2): the
+ * packed rows of B images (offsets z_off, int32[B+1], as the merges write them) to a
+ * dense [B][P][row_bytes] array, image b's rows first and zero rows after them:
+ *   out[b][k] = z[z_off[b] + k] for k < min(n_b, P), zeros for n_b <= k < P.
+ * For the parts of a model that need equal-length images (batched attention with a
+ * key mask), while the per-token parts keep the packed rows. Rows are copied as
+ * bytes: row_bytes a positive multiple of 16 (any dtype, several heads' features in
+ * one row, ...). P is the caller's choice, usually the batch's largest n_b (read from
+ * z_off) or N. Errors: MPM_ERR_INVALID_ARG for B < 1, P < 1, a row size that is not a
+ * positive multiple of 16 or bad pointers; MPM_ERR_UNSUPPORTED for B, P or rows above
+ * the maxima (MPM_MAX_B, MPM_MAX_N, 4 * MPM_MAX_D bytes).
+ */
+int mpm_pad(const void* z, const int32_t* z_off, int32_t B, int32_t P, int32_t row_bytes, void* out, void* stream);
+
+/* The inverse of mpm_pad: z[z_off[b] + k] = padded[b][k] for k < min(n_b, P); padded
+ * rows k >= n_b are not read. Arguments and errors as mpm_pad. */
+int mpm_unpad(const void* padded, const int32_t* z_off, int32_t B, int32_t P, int32_t row_bytes, void* z,
+              void* stream);
+
+/*
  * mpm_merge for callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid allocation): the workspace
  * is a file-scope device array of MPM_NOALLOC_SCRATCH_BYTES that each GPU the

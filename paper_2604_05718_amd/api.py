@@ -12,6 +12,7 @@ Token layouts (see include/mpm.h):
 from __future__ import annotations
 
 import ctypes
+import math
 from dataclasses import dataclass
 
 import torch
@@ -235,6 +236,30 @@ def merge_local(x, grid_w: int, window: int, x_off=None, N=None, pos=None, ws=No
                                                               int(window), _p(y), _p(y_off), _p(y_pos), _p(m), _p(ws),
                                                               ws.numel(), None, None, _stream()))
     return Merged(y, y_off, m, ws, B, N, None, y_pos)
+
+
+def pad(z, z_off, P: int, out=None):
+    """Packed rows z [R, ...] (offsets z_off [B+1]) to [B, P, ...]: image b's rows
+    first, zero rows after them (mpm_pad; the row is copied as bytes)."""
+    B = z_off.numel() - 1
+    row_bytes = math.prod(z.shape[1:]) * z.element_size()
+    if out is None:
+        out = torch.empty((B, P) + tuple(z.shape[1:]), dtype=z.dtype, device=z.device)
+    _lib.check("mpm_pad", _lib.load().mpm_pad(_p(z), _p(z_off), B, int(P), int(row_bytes), _p(out), _stream()))
+    return out
+
+
+def unpad(padded, z_off, out=None, rows: int | None = None):
+    """The inverse of pad: [B, P, ...] back to packed rows (mpm_unpad); ``out`` (or a new
+    tensor of ``rows`` rows, default B * P) receives them at the offsets z_off."""
+    B, P = padded.shape[:2]
+    row_bytes = math.prod(padded.shape[2:]) * padded.element_size()
+    if out is None:
+        out = torch.empty((rows if rows is not None else B * P,) + tuple(padded.shape[2:]), dtype=padded.dtype,
+                          device=padded.device)
+    _lib.check("mpm_unpad", _lib.load().mpm_unpad(_p(padded), _p(z_off), B, int(P), int(row_bytes), _p(out),
+                                                  _stream()))
+    return out
 
 
 def compose(map_a, map_b, out=None):

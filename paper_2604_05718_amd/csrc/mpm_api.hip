@@ -389,6 +389,25 @@ int mpm_merge_local(const void* x, const int32_t* x_off, const int32_t* pos, int
     return hip_status(e);
 }
 
+int mpm_pad(const void* z, const int32_t* z_off, int32_t B, int32_t P, int32_t row_bytes, void* out, void* stream)
+{
+    if (B < 1 || P < 1 || row_bytes < 16 || row_bytes % 16 != 0) return MPM_ERR_INVALID_ARG;
+    if (B > MPM_MAX_B || P > MPM_MAX_N || row_bytes > MPM_MAX_D * 4) return MPM_ERR_UNSUPPORTED;
+    if (!ok_rows_ptr(z) || !ok_int_ptr(z_off) || !ok_rows_ptr(out)) return MPM_ERR_INVALID_ARG;
+    MPM_LAUNCH_GATE();
+    return hip_status(mpm::launch_pad(z, z_off, B, P, row_bytes, out, false, as_stream(stream)));
+}
+
+int mpm_unpad(const void* padded, const int32_t* z_off, int32_t B, int32_t P, int32_t row_bytes, void* z,
+              void* stream)
+{
+    if (B < 1 || P < 1 || row_bytes < 16 || row_bytes % 16 != 0) return MPM_ERR_INVALID_ARG;
+    if (B > MPM_MAX_B || P > MPM_MAX_N || row_bytes > MPM_MAX_D * 4) return MPM_ERR_UNSUPPORTED;
+    if (!ok_rows_ptr(padded) || !ok_int_ptr(z_off) || !ok_rows_ptr(z)) return MPM_ERR_INVALID_ARG;
+    MPM_LAUNCH_GATE();
+    return hip_status(mpm::launch_pad(padded, z_off, B, P, row_bytes, z, true, as_stream(stream)));
+}
+
 int mpm_compose(const int32_t* map_a, const int32_t* map_b, int32_t B, int32_t N, int32_t* map_ab, void* stream)
 {
     const int s = check_shape(B, N);

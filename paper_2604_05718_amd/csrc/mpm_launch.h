@@ -57,6 +57,11 @@ hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const int3
                                  int B, int N, int D, int dt, float* pv, int32_t* pi, hipStream_t stream,
                                  hipEvent_t start, hipEvent_t stop);
 
+// Padded batch layout: packed rows (offsets z_off) to [B][P] rows of rowbytes bytes, zero
+// rows past each image (unpad = false), or back to the packed layout (unpad = true).
+hipError_t launch_pad(const void* z, const int32_t* z_off, int B, int P, long rowbytes, void* out, bool unpad,
+                      hipStream_t stream);
+
 hipError_t launch_compose(const int32_t* map_a, const int32_t* map_b, int B, int N,
                           int32_t* map_ab, hipStream_t stream);
 

@@ -264,6 +264,38 @@ __global__ __launch_bounds__(kRowThreads) void unmerge_kernel(
         [&](long r, int c, u32x4 v) { store16_stream(oimg + r * rowbytes + c * 16, v); });
 }
 
+// Padded batch layout: out[b][k] = z[z_off[b] + k] for k < n_b, zeros for n_b <= k < P
+// (P = padded rows per image), one 16-byte vector per lane and step; with UNPAD the
+// copy goes back, out packed from a padded z, rows k >= n_b not read.
+template <bool UNPAD>
+__global__ __launch_bounds__(kRowThreads) void pad_kernel(const uint8_t* __restrict__ z,
+                                                          const int32_t* __restrict__ z_off, int P, long rowbytes,
+                                                          int rows_per_block, uint8_t* __restrict__ out)
+{
+    const int b = blockIdx.y;
+    const int o = z_off[b];
+    const int n = min(max(z_off[b + 1] - o, 0), P);
+    const int r0 = blockIdx.x * rows_per_block;
+    const int r1 = min(UNPAD ? n : P, r0 + rows_per_block);
+    if (r0 >= r1) return;
+    const int vpr = (int)(rowbytes / 16);
+    const uint8_t* packed_z = z + (long)o * rowbytes;          // pad: the image's packed rows
+    const uint8_t* padded_z = z + (long)b * P * rowbytes;      // unpad: the image's padded rows
+    uint8_t* padded_out = out + (long)b * P * rowbytes;
+    uint8_t* packed_out = out + (long)o * rowbytes;
+    for_each_vec_batched<kGatherBatch>((long)r0 * vpr, (long)r1 * vpr, vpr,
+        [&](long r, int c) {
+            u32x4 v = {0u, 0u, 0u, 0u};
+            if (UNPAD) v = load16(padded_z + r * rowbytes + c * 16);
+            else if (r < n) v = load16(packed_z + r * rowbytes + c * 16);
+            return v;
+        },
+        [&](long r, int c, u32x4 v) {
+            if (UNPAD) store16(packed_out + r * rowbytes + c * 16, v);
+            else store16(padded_out + r * rowbytes + c * 16, v);
+        });
+}
+
 int rows_per_block_for(long rowbytes, long block_bytes = kRowBytesPerBlock)
 {
     const long r = block_bytes / rowbytes;
@@ -325,6 +357,24 @@ hipError_t launch_unmerge(const void* z, const int32_t* z_off, const int32_t* ma
     else
         hipLaunchKernelGGL(unmerge_kernel<F32>, grid, dim3(kRowThreads), 0, stream, zp, z_off, map, map2, map_ab, sp, E,
                            N, D, rpb, op);
+    return hipGetLastError();
+}
+
+}  // namespace mpm
+
+namespace mpm {
+
+hipError_t launch_pad(const void* z, const int32_t* z_off, int B, int P, long rowbytes, void* out, bool unpad,
+                      hipStream_t stream)
+{
+    const int rpb = rows_per_block_for(rowbytes, kGatherBytesPerBlock);
+    dim3 grid((P + rpb - 1) / rpb, B);
+    const uint8_t* zp = static_cast<const uint8_t*>(z);
+    uint8_t* op = static_cast<uint8_t*>(out);
+    if (unpad)
+        hipLaunchKernelGGL(pad_kernel<true>, grid, dim3(kRowThreads), 0, stream, zp, z_off, P, rowbytes, rpb, op);
+    else
+        hipLaunchKernelGGL(pad_kernel<false>, grid, dim3(kRowThreads), 0, stream, zp, z_off, P, rowbytes, rpb, op);
     return hipGetLastError();
 }
 
