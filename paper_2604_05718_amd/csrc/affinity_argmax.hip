@@ -622,6 +622,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     };
 
     Item ii = find(slot);  // issue cursor
+    if (ii.k >= nitems) return;  // no work for this slot (uniform over the workgroup)
     Offsets ioff = offsets_of(ii);
     int ichunk = 0;
     int issued = 0;
@@ -636,8 +637,10 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         isb = lds + (issued % STAGES) * STAGE_BYTES;
         ibase = x + (long)ii.row0 * rowbytes + (long)ichunk * CB;   // uniform
     };
+    // Once the issue cursor is past its last item the loads go on, unconditionally (no branch
+    // per load in the K loop): they re-read rows of the last item (valid addresses) into the
+    // ring slot after the last chunk, which nothing reads any more.
     auto issue_part = [&](int i) {
-        if (!iact) return;
         const uint32_t off = ioff.v[i];
         const uint32_t m0 =
             (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)(isb + (wave + WAVES * i) * RPI * CB);
@@ -1037,6 +1040,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         fetch_inv(ci);
         if constexpr (HALVES) lq_off = (ci.qbase - ci.cbase + wq * NT * 32 + lrow) * CB;
     }
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // the trailing loads land before the workgroup's LDS is released
 }
 
 // Persistent-kernel shape: 256 candidates x 256 queries on 8 waves, 128-byte K

@@ -11,10 +11,11 @@
 // scan of the paper. Partners then copy the id of their (lower-index)
 // representative.
 //
-// Offsets: each image's workgroup stores its cluster count in y_off[b+1]. With an
-// arrival counter (the workspace's sync region), the workgroup that finishes last
-// turns the counts into offsets in place, so the pair average reads each image's
-// offset once instead of summing the counts before it; without one, a second
+// Offsets: each image's workgroup stores its cluster count in y_off[b+1] as soon as
+// its scan has it. With an arrival counter (the workspace's sync region), the
+// workgroup whose arrival is counted last turns the counts into offsets in place
+// once its own writes are issued, so the pair average reads each image's offset
+// once instead of summing the counts before it; without one, a second
 // one-workgroup launch does it. No workgroup ever waits for another.
 #include "mpm_device.h"
 #include "mpm_launch.h"
@@ -162,6 +163,14 @@ __global__ __launch_bounds__(kCompactThreads) void pair_compact_kernel(
     }
     int total;
     int id = block_exclusive_scan(reps, wave_sum, &total);
+    // The image's count is final here: publish it and count the arrival now, so that the
+    // atomic's round trip overlaps the src and map writes below (its result is read last).
+    int arrived = 0;
+    if (sync != nullptr && tid == 0) {
+        store_coherent(y_off + b + 1, total);
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the count is at the coherence point
+        arrived = __hip_atomic_fetch_add(sync + kDoneSlot, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     for (int i = i0; i < i1; ++i) {
         const int j = nbl[i];
         const bool mutual = is_mutual(nbl, i, j, n);
@@ -187,11 +196,7 @@ __global__ __launch_bounds__(kCompactThreads) void pair_compact_kernel(
         if (tid == 0) y_off[b + 1] = total;
         return;
     }
-    if (tid == 0) {
-        store_coherent(y_off + b + 1, total);
-        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the count is at the coherence point
-        last = __hip_atomic_fetch_add(sync + kDoneSlot, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == B - 1;
-    }
+    if (tid == 0) last = arrived == B - 1;
     __syncthreads();
     if (!last) return;
     scan_offsets<true>(y_off, B, wave_sum);
