@@ -688,12 +688,27 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x16{};
-    float ss[MT];
+    // Norm sums (rows not given): wave (wc, wq) sums candidate m-tiles wq, wq + WQ, ... and,
+    // in the symmetric schedule, query n-tiles wc, wc + WC, ... It reads those fragments from
+    // LDS a second time, before each k-group's MFMAs (own_c / own_q: their offsets in a stage,
+    // before the k column), and sums them after the MFMAs under one uniform branch per k-group.
+    // Picking them out of its registers by wave index instead took a branch per tile in the K
+    // loop, which cost 5-8% of the launch with norms summed. An index past the wave's tiles
+    // reads its last tile, whose sum is unused.
+    constexpr int NSC = (MT + WQ - 1) / WQ;
+    constexpr int NSQ = SYM ? (NT + WC - 1) / WC : 1;
+    float ss[NSC], sq[NSQ];
+    int own_c[NSC], own_q[NSQ];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) ss[mt] = 0.0f;
-    float sq[NT];  // query norms (symmetric schedule only)
+    for (int j = 0; j < NSC; ++j) {
+        ss[j] = 0.0f;
+        own_c[j] = lc_off + min(wq + j * WQ, MT - 1) * 32 * CB;
+    }
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) sq[nt] = 0.0f;
+    for (int j = 0; j < NSQ; ++j) {
+        sq[j] = 0.0f;
+        own_q[j] = min(wc + j * WC, NT - 1) * 32 * CB;  // from lq_off
+    }
     // One load part before every PSTEP-th MFMA of a chunk: spread over all of the chunk's MFMAs
     // with STAGES >= 3, over the first half with two stages (those loads must land before the
     // chunk ends).
@@ -702,7 +717,18 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     static_assert(PSPAN >= 1, "load parts per MFMA");
     constexpr int PSTEP = PSPAN >= LOADS ? PSPAN / LOADS : 1;              // MFMAs between load slots
     constexpr int PPER = PSPAN >= LOADS ? 1 : (LOADS + PSPAN - 1) / PSPAN;  // loads per slot (small tiles)
-    auto mma_issue = [&](const u32x4 (&fa)[MT], const u32x4 (&fq)[NT], int g) {
+    auto mma_issue = [&](const u32x4 (&fa)[MT], const u32x4 (&fq)[NT], int chunk, int g) {
+        u32x4 oc[NSC], oq[NSQ];
+        {
+            const uint8_t* sb = lds + (chunk % STAGES) * STAGE_BYTES;
+            const int col = ((2 * g + khalf) ^ sw) << 4;
+#pragma unroll
+            for (int j = 0; j < NSC; ++j) oc[j] = *reinterpret_cast<const u32x4*>(sb + own_c[j] + col);
+            if constexpr (SYM) {
+#pragma unroll
+                for (int j = 0; j < NSQ; ++j) oq[j] = *reinterpret_cast<const u32x4*>(sb + lq_off + own_q[j] + col);
+            }
+        }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
@@ -715,14 +741,14 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                 }
                 Mfma<S>::mma(acc[mt][nt], fa[mt], fq[nt]);
             }
-            // Candidate norms: m-tile mt is summed by the wave with wq == mt % WQ only.
-            if (!given && mt % WQ == wq) ss[mt] = Mfma<S>::sumsq(fa[mt], ss[mt]);
         }
-        if constexpr (SYM) {
-            // Query norms, for the reverse direction: n-tile nt is summed by the wave with wc == nt % WC.
+        if (!given) {
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-                if (!given && nt % WC == wc) sq[nt] = Mfma<S>::sumsq(fq[nt], sq[nt]);
+            for (int j = 0; j < NSC; ++j) ss[j] = Mfma<S>::sumsq(oc[j], ss[j]);
+            if constexpr (SYM) {
+#pragma unroll
+                for (int j = 0; j < NSQ; ++j) sq[j] = Mfma<S>::sumsq(oq[j], sq[j]);
+            }
         }
     };
     // vmcnt(n) with expcnt and lgkmcnt unconstrained.
@@ -784,8 +810,8 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
             } else if (STAGES >= 3 && issued > consumed + 1) {
                 read_frags(fa0, fq0, consumed + 1, 0);
             }
-            if ((g & 1) == 0) mma_issue(fa0, fq0, g);
-            else mma_issue(fa1, fq1, g);
+            if ((g & 1) == 0) mma_issue(fa0, fq0, consumed, g);
+            else mma_issue(fa1, fq1, consumed, g);
         }
         issue_end();
         ++consumed;
@@ -797,22 +823,26 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
             else if (SYM && tid < CT + QT) inv_q[SYM ? tid - CT : 0] = inv_pre;
         } else {
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                if (mt % WQ != wq) continue;
-                const float t = ss[mt] + __shfl_xor(ss[mt], 32);  // lanes l, l+32: the two k halves
-                ss[mt] = 0.0f;
+            for (int j = 0; j < NSC; ++j) {
+                const int mt = wq + j * WQ;
+                if (mt >= MT) break;
+                const float t = ss[j] + __shfl_xor(ss[j], 32);  // lanes l, l+32: the two k halves
                 if (khalf == 0) inv_c[wc * MT * 32 + mt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
             }
             if constexpr (SYM) {
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt) {
-                    if (nt % WC != wc) continue;
-                    const float t = sq[nt] + __shfl_xor(sq[nt], 32);
-                    sq[nt] = 0.0f;
+                for (int j = 0; j < NSQ; ++j) {
+                    const int nt = wc + j * WC;
+                    if (nt >= NT) break;
+                    const float t = sq[j] + __shfl_xor(sq[j], 32);
                     if (khalf == 0) inv_q[wq * NT * 32 + nt * 32 + lrow] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
                 }
             }
         }
+#pragma unroll
+        for (int j = 0; j < NSC; ++j) ss[j] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < NSQ; ++j) sq[j] = 0.0f;
         lds_barrier();
         const float* iv = inv_c;
         const int n = ci.n;
