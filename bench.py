@@ -33,9 +33,9 @@ METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak
 # rocprofv3 FETCH_SIZE / WRITE_SIZE runs on each workload, calibrated with a copy
 # kernel (profiles/<workload>_rocprof.md). Valid only for the kernel source it was
 # measured on, with the default schedule.
-TRAFFIC = {"source_sha256": "d2f6621e8438d01006479306f60947d0499c50a2f6ad61b68431842fd9c56746",
-           "bytes_per_launch": {"vit_ti_512": 6555874, "vit_s_512": 24996198, "vit_b_512": 149457124,
-                                "vit_l_1024": 499851763, "stress_768": 178310894}}
+TRAFFIC = {"source_sha256": "1967554c226163b6f301b1f155d02746ae7bf2128d5232fc2e745da8306674cb",
+           "bytes_per_launch": {"vit_ti_512": 6552809, "vit_s_512": 25842442, "vit_b_512": 151348198,
+                                "vit_l_1024": 510512743, "stress_768": 182734041}}
 
 
 def log(*a):
