@@ -127,6 +127,38 @@ def test_other_entry_points_reject(lib):
     assert lib.mpm_last_hip_error() == 0
 
 
+def test_pad_unpad_and_local_reject(lib):
+    """mpm_pad / mpm_unpad and mpm_merge_local return their argument errors before any
+    device work: sizes, row bytes that are not whole 16-byte vectors, NULL or misaligned
+    pointers, a grid or window the locality constraint cannot take, a short workspace."""
+    for fn in (lib.mpm_pad, lib.mpm_unpad):
+        assert fn(A, A, 0, 8, 64, A2, None) == 1             # B < 1
+        assert fn(A, A, 2, 0, 64, A2, None) == 1             # P < 1
+        assert fn(A, A, 2, 8, 8, A2, None) == 1              # row_bytes < 16
+        assert fn(A, A, 2, 8, 40, A2, None) == 1             # row_bytes % 16
+        assert fn(A, None, 2, 8, 64, A2, None) == 1          # z_off NULL
+        assert fn(MIS, A, 2, 8, 64, A2, None) == 1           # rows misaligned
+        assert fn(A, A, 2, 8, 64, MIS, None) == 1
+        assert fn(A, A, 65536, 8, 64, A2, None) == 2         # B > MPM_MAX_B
+        assert fn(A, A, 2, 16385, 64, A2, None) == 2         # P > MPM_MAX_N
+    ws = ctypes.c_size_t(1 << 30)
+    odd = ctypes.c_void_p(0x10002)
+    ok = dict(pos=None, grid_w=8, window=1, y_pos=A2)
+
+    def local(**kw):
+        a = dict(ok, **kw)
+        return lib.mpm_merge_local(A, None, a["pos"], 2, 64, 64, 1, a["grid_w"], a["window"], A2, A2, a["y_pos"],
+                                   A2, A2, a.get("ws", ws), None, None, None)
+    assert local(grid_w=0) == 1
+    assert local(grid_w=16385) == 1
+    assert local(window=-1) == 1
+    assert local(y_pos=None) == 1
+    assert local(pos=odd) == 1                                # positions misaligned
+    assert local(ws=16) == 3                                  # workspace too small
+    assert lib.mpm_merge_local(A, None, None, 2, 64, 63, 1, 8, 1, A2, A2, A2, A2, A2, ws, None, None, None) == 1
+    assert lib.mpm_last_hip_error() == 0
+
+
 def test_given_norms_reject(lib):
     """Given inverse norms: a misaligned pointer, and rows the norm-taking kernels do
     not cover, are rejected by every affinity entry point."""
