@@ -471,16 +471,25 @@ __host__ __device__ inline int deferred_diagonals(int nimg, int nb, int slots)
 // reverse direction, so the two halves write disjoint query partials, and each score
 // comes from the same MFMA sequence as in a whole block.
 //
+// LOCAL: the locality constraint of Sec. 5 on the full schedule. A work item is a query
+// block with every candidate tile its window band reaches ([tlo, thi], found from the
+// positions at the block and tile boundaries, as in the register-staged kernel); the item
+// runs its tiles one after the other through the same ring (one K loop per tile), keeps
+// each query's running best across them in registers, masks every score by the window
+// test, and writes one partial per query (tile slot 0, tile width N). Positions (win.pos,
+// null: the token's index) are fetched per tile while its K loop runs, as given norms are.
+//
 // xinv (may be null): the inverse row norms 1 / max(||x_j||, 1e-12), one float per row
 // packed like x, given instead of summed from the fragments in the K loop (vector ALU
 // work in the K loop adds to its time about one for one, and these sums are a tenth of
 // it). A run-time choice in one kernel, not a second build: the two insertions of a
 // schedule then run the same code, which a second build would evict from the
 // instruction cache at every switch (that cost 3-4% of the other insertion's launch).
-template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES, bool SYM, bool HALVES = false>
+template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES, bool SYM, bool HALVES = false,
+          bool LOCAL = false>
 __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  // 2 waves per SIMD
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int T, int xcds,
-    int slots, float* __restrict__ pv, int32_t* __restrict__ pi, const float* __restrict__ xinv)
+    int slots, float* __restrict__ pv, int32_t* __restrict__ pi, const float* __restrict__ xinv, Window win)
 {
     constexpr int THREADS = WC * WQ * kWave;
     constexpr int WAVES = WC * WQ;
@@ -507,6 +516,10 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     __shared__ __attribute__((aligned(16))) float inv_q[SYM ? QT : 1];
     __shared__ float red_cv[SYM ? WQ : 1][SYM ? CT : 1];
     __shared__ int32_t red_ci[SYM ? WQ : 1][SYM ? CT : 1];
+    // LOCAL: grid row [0] and column [1] of the item's candidates (0 .. CT-1) and queries (CT ..).
+    __shared__ __attribute__((aligned(16))) int32_t win_rc[2][LOCAL ? CT + QT : 1];
+    static_assert(!LOCAL || (!SYM && !HALVES && QT == CT && CT + QT <= WC * WQ * kWave),
+                  "window items: full schedule, square blocks, one position per thread");
     static_assert(!SYM || QT == CT, "the symmetric schedule pairs equal blocks");
     static_assert(CT + (SYM ? QT : 0) <= THREADS, "one given inverse norm per thread and item");
     // Uniform. Bfloat16 rows only: the float32 kernels would spill a register with it.
@@ -524,7 +537,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     const int slot = blockIdx.x / xcds;
     const int nqb = (N + QT - 1) / QT;
     const int nct = (N + CT - 1) / CT;  // candidate tiles per image (T, the slot stride, may be larger)
-    const int per_img = SYM ? nqb * (nqb + 1) / 2 : nqb * nct;
+    const int per_img = LOCAL ? nqb : (SYM ? nqb * (nqb + 1) / 2 : nqb * nct);
     const int nimg = (B - group + xcds - 1) / xcds;
     static_assert(!HALVES || (!SYM && 2 * QT == CT), "half items: forward only, half a block of queries");
     constexpr bool SPLIT = SYM && STAGES == 2;  // the layouts the second launch exists for
@@ -539,6 +552,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     // Item cursor; all fields are uniform over the workgroup.
     struct Item {
         int k, b, qbase, cbase, n, row0;
+        int thi;  // LOCAL: the last candidate tile of the item's band (cbase walks up to it)
     };
     auto find = [&](int k) {
         Item it;
@@ -556,6 +570,10 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                 }
                 t = qb;
                 qbase = qb * CT + (k & 1) * QT;
+            } else if (LOCAL) {  // query block qb of image ib; its band's first tile is found below
+                ib = k / nqb;
+                t = k - ib * nqb;
+                qbase = t * QT;
             } else if (SYM) {  // blocks qb <= t of the upper triangle, row by row, minus deferred diagonals
                 int w;
                 if (k < upto_dimg) {
@@ -588,11 +606,33 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
             const int n = x_off ? x_off[b + 1] - row0 : N;
             if (qbase < n && t * CT < n) {
                 it.k = k; it.b = b; it.qbase = qbase; it.cbase = t * CT; it.n = n; it.row0 = row0;
+                it.thi = t;
+                if constexpr (LOCAL) {
+                    // Candidate tiles whose grid rows can meet the block's window rows.
+                    auto grid_row = [&](int i) { return (win.pos ? win.pos[row0 + i] : i) / win.grid_w; };
+                    const int r_first = grid_row(qbase), r_last = grid_row(min(qbase + QT, n) - 1);
+                    int tlo = 0, thi = (n - 1) / CT;
+                    while (tlo < thi && grid_row(min((tlo + 1) * CT, n) - 1) < r_first - win.radius) ++tlo;
+                    while (thi > tlo && grid_row(thi * CT) > r_last + win.radius) --thi;
+                    it.cbase = tlo * CT;
+                    it.thi = thi;
+                }
                 return it;
             }
         }
-        it.k = nitems; it.b = 0; it.qbase = 0; it.cbase = 0; it.n = 1; it.row0 = 0;
+        it.k = nitems; it.b = 0; it.qbase = 0; it.cbase = 0; it.n = 1; it.row0 = 0; it.thi = 0;
         return it;
+    };
+    // The work after `it`: its next band tile (LOCAL), else the slot's next item.
+    auto next_of = [&](const Item& it) {
+        if constexpr (LOCAL) {
+            if (it.cbase < it.thi * CT) {
+                Item nx = it;
+                nx.cbase += CT;
+                return nx;
+            }
+        }
+        return find(it.k + slots);
     };
 
     // Swizzle of the 16-byte column slot for a row (see the layout note above).
@@ -653,7 +693,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         ++issued;
         if (++ichunk == nchunks) {
             ichunk = 0;
-            ii = find(ii.k + slots);
+            ii = next_of(ii);
             if (ii.k < nitems) ioff = offsets_of(ii);
         }
     };
@@ -778,7 +818,25 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
             if (tid < CT || (SYM && tid < CT + QT)) inv_pre = xinv[it.row0 + min(r, it.n - 1)];
         }
     };
+    // LOCAL: thread t fetches the grid position of candidate row t or query row t - CT of
+    // the compute cursor's tile; it goes to win_rc at the tile's end.
+    int pos_pre = 0;
+    auto fetch_pos = [&](const Item& it) {
+        if (LOCAL && it.k < nitems && tid < CT + QT) {
+            const int r = min(tid < CT ? it.cbase + tid : it.qbase + tid - CT, it.n - 1);
+            pos_pre = win.pos ? win.pos[it.row0 + r] : r;
+        }
+    };
     fetch_inv(ci);
+    fetch_pos(ci);
+    // LOCAL: each query's best so far over the item's earlier tiles (this lane's n-tiles).
+    float bv_run[LOCAL ? NT : 1];
+    int32_t bi_run[LOCAL ? NT : 1];
+#pragma unroll
+    for (int nt = 0; nt < (LOCAL ? NT : 1); ++nt) {
+        bv_run[nt] = -__builtin_inff();
+        bi_run[nt] = -1;
+    }
     int cchunk = 0;
     int consumed = 0;
     while (ci.k < nitems) {
@@ -843,6 +901,12 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         for (int j = 0; j < NSC; ++j) ss[j] = 0.0f;
 #pragma unroll
         for (int j = 0; j < NSQ; ++j) sq[j] = 0.0f;
+        if constexpr (LOCAL) {
+            if (tid < CT + QT) {
+                win_rc[0][tid] = pos_pre / win.grid_w;
+                win_rc[1][tid] = pos_pre % win.grid_w;
+            }
+        }
         lds_barrier();
         const float* iv = inv_c;
         const int n = ci.n;
@@ -866,9 +930,20 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         int32_t bi[NT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-            bv[nt] = -__builtin_inff();
-            bi[nt] = -1;
+            bv[nt] = LOCAL ? bv_run[LOCAL ? nt : 0] : -__builtin_inff();
+            bi[nt] = LOCAL ? bi_run[LOCAL ? nt : 0] : -1;
         }
+        // LOCAL: this lane's query's grid row and column per n-tile; the window test is
+        // |row_j - row_q| <= radius and |col_j - col_q| <= radius, as unsigned compares.
+        int q_r[LOCAL ? NT : 1], q_c[LOCAL ? NT : 1];
+        if constexpr (LOCAL) {
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+                q_r[nt] = win_rc[0][CT + wq * NT * 32 + nt * 32 + lrow] - win.radius;
+                q_c[nt] = win_rc[1][CT + wq * NT * 32 + nt * 32 + lrow] - win.radius;
+            }
+        }
+        const uint32_t wspan = 2u * (uint32_t)win.radius;
         // This lane's own row inside a 32-row tile, as an accumulator element (if it holds it).
         const int self_r = (((lrow >> 2) & 1) == khalf) ? 4 * (lrow >> 3) + (lrow & 3) : -1;
 #pragma unroll
@@ -896,6 +971,20 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                 if (diag && wc * MT + mt == self_tile0 + wq * NT + nt) {  // the tile holding each lane's own query
 #pragma unroll
                     for (int r = 0; r < 16; ++r) sc[r] = r == self_r ? -__builtin_inff() : sc[r];
+                }
+                if constexpr (LOCAL) {
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int jl = wc * MT * 32 + mt * 32 + 8 * g + 4 * khalf;
+                        const int4 cr = *reinterpret_cast<const int4*>(&win_rc[0][jl]);
+                        const int4 cc = *reinterpret_cast<const int4*>(&win_rc[1][jl]);
+                        const int crv[4] = {cr.x, cr.y, cr.z, cr.w}, ccv[4] = {cc.x, cc.y, cc.z, cc.w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const bool in = (uint32_t)(crv[e] - q_r[nt]) <= wspan && (uint32_t)(ccv[e] - q_c[nt]) <= wspan;
+                            sc[4 * g + e] = in ? sc[4 * g + e] : -__builtin_inff();
+                        }
+                    }
                 }
                 float v8[8];
                 int r8[8];
@@ -1013,61 +1102,75 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x16{};  // the next item starts from zero
-        // Merge the two lane halves, then the WC candidate waves (larger score, then smaller index).
+        // LOCAL: between the tiles of an item only the running best is kept; the lanes,
+        // waves and the partial are merged and written after its last tile.
+        bool item_end = true;
+        if constexpr (LOCAL) {
+            item_end = ci.cbase >= ci.thi * CT;
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-            float v = bv[nt];
-            int32_t i = bi[nt];
-            const float ov = __shfl_xor(v, 32);
-            const int32_t oi = __shfl_xor(i, 32);
-            if (ov > v || (ov == v && (uint32_t)oi < (uint32_t)i)) {
-                v = ov;
-                i = oi;
-            }
-            if (khalf == 0) {
-                const int ql = wq * NT * 32 + nt * 32 + lrow;
-                red_v[wc][ql] = v;
-                red_i[wc][ql] = i;
+            for (int nt = 0; nt < NT; ++nt) {
+                bv_run[nt] = item_end ? -__builtin_inff() : bv[nt];
+                bi_run[nt] = item_end ? -1 : bi[nt];
             }
         }
-        lds_barrier();
-        const int t = cb / CT;
-        for (int ql = tid; ql < QT; ql += THREADS) {
-            const int qi = ci.qbase + ql;
-            if (qi >= n) continue;
-            float v = red_v[0][ql];
-            int32_t i = red_i[0][ql];
+        if (item_end) {
+            // Merge the two lane halves, then the WC candidate waves (larger score, then smaller index).
 #pragma unroll
-            for (int w = 1; w < WC; ++w) {
-                const float ov = red_v[w][ql];
-                const int32_t oi = red_i[w][ql];
+            for (int nt = 0; nt < NT; ++nt) {
+                float v = bv[nt];
+                int32_t i = bi[nt];
+                const float ov = __shfl_xor(v, 32);
+                const int32_t oi = __shfl_xor(i, 32);
                 if (ov > v || (ov == v && (uint32_t)oi < (uint32_t)i)) {
                     v = ov;
                     i = oi;
                 }
+                if (khalf == 0) {
+                    const int ql = wq * NT * 32 + nt * 32 + lrow;
+                    red_v[wc][ql] = v;
+                    red_i[wc][ql] = i;
+                }
             }
-            const long o = ((long)ci.b * T + t) * N + qi;
-            pv[o] = v;
-            pi[o] = i;
-        }
-        if (rev) {
-            // Candidate rows of the tile over the query block: tile slot qbase / QT of their partials.
-            const int tq = ci.qbase / QT;
-            for (int jl = tid; jl < CT; jl += THREADS) {
-                const int j = cb + jl;
-                if (j >= n) continue;
-                float v = red_cv[0][jl];
-                int32_t i = red_ci[0][jl];
+            lds_barrier();
+            const int t = LOCAL ? 0 : cb / CT;  // LOCAL: one partial per query, tile slot 0
+            for (int ql = tid; ql < QT; ql += THREADS) {
+                const int qi = ci.qbase + ql;
+                if (qi >= n) continue;
+                float v = red_v[0][ql];
+                int32_t i = red_i[0][ql];
 #pragma unroll
-                for (int w = 1; w < WQ; ++w) merge_pair(v, i, v, i, red_cv[w][jl], red_ci[w][jl]);
-                const long o = ((long)ci.b * T + tq) * N + j;
+                for (int w = 1; w < WC; ++w) {
+                    const float ov = red_v[w][ql];
+                    const int32_t oi = red_i[w][ql];
+                    if (ov > v || (ov == v && (uint32_t)oi < (uint32_t)i)) {
+                        v = ov;
+                        i = oi;
+                    }
+                }
+                const long o = ((long)ci.b * T + t) * N + qi;
                 pv[o] = v;
                 pi[o] = i;
             }
+            if (rev) {
+                // Candidate rows of the tile over the query block: tile slot qbase / QT of their partials.
+                const int tq = ci.qbase / QT;
+                for (int jl = tid; jl < CT; jl += THREADS) {
+                    const int j = cb + jl;
+                    if (j >= n) continue;
+                    float v = red_cv[0][jl];
+                    int32_t i = red_ci[0][jl];
+#pragma unroll
+                    for (int w = 1; w < WQ; ++w) merge_pair(v, i, v, i, red_cv[w][jl], red_ci[w][jl]);
+                    const long o = ((long)ci.b * T + tq) * N + j;
+                    pv[o] = v;
+                    pi[o] = i;
+                }
+            }
         }
         cchunk = 0;
-        ci = find(ci.k + slots);
+        ci = next_of(ci);
         fetch_inv(ci);
+        fetch_pos(ci);
         if constexpr (HALVES) lq_off = (ci.qbase - ci.cbase + wq * NT * 32 + lrow) * CB;
     }
     __builtin_amdgcn_s_waitcnt(0x0F70);  // the trailing loads land before the workgroup's LDS is released
@@ -1120,28 +1223,29 @@ bool defers_diagonals(int B, int N, int xcds, int slots)
     return false;
 }
 
-template <class S, int WC, int WQ, int MT, int NT, bool SYM>
+template <class S, int WC, int WQ, int MT, int NT, bool SYM, bool LOCAL = false>
 void launch_persistent(const void* x, const int32_t* x_off, const float* xinv, int B, int N, int D, int T, int xcds,
-                       int groups, float* pv, int32_t* pi, hipStream_t stream, hipEvent_t start, hipEvent_t stop)
+                       int groups, float* pv, int32_t* pi, hipStream_t stream, hipEvent_t start, hipEvent_t stop,
+                       Window win = Window{nullptr, 1, 0})
 {
     const uint8_t* xb = static_cast<const uint8_t*>(x);
     if (((long)D * S::kBytes) % kPCB2 == 0) {
         // The symmetric schedule's deferred diagonal blocks, as half blocks, in a second launch
         // (one item per slot); the timing events then span both.
         const bool halves = SYM && defers_diagonals(B, N, xcds, groups / xcds);
-        hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB2, 2, SYM>), dim3(groups),
+        hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB2, 2, SYM, false, LOCAL>), dim3(groups),
                               dim3(WC * WQ * kWave), 0, stream, start, halves ? nullptr : stop, 0, xb, x_off, B, N,
-                              D, T, xcds, groups / xcds, pv, pi, xinv);
+                              D, T, xcds, groups / xcds, pv, pi, xinv, win);
         if constexpr (SYM) {
             if (halves)
                 hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT / 2, kPCB2, 2, false, true>),
                                       dim3(groups), dim3(WC * WQ * kWave), 0, stream, nullptr, stop, 0, xb, x_off, B,
-                                      N, D, T, xcds, groups / xcds, pv, pi, xinv);
+                                      N, D, T, xcds, groups / xcds, pv, pi, xinv, win);
         }
     } else
-        hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB, 4, SYM>), dim3(groups),
+        hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB, 4, SYM, false, LOCAL>), dim3(groups),
                               dim3(WC * WQ * kWave), 0, stream, start, stop, 0, xb, x_off, B, N, D, T, xcds,
-                              groups / xcds, pv, pi, xinv);
+                              groups / xcds, pv, pi, xinv, win);
 }
 
 template <class S, int WC, int WQ, int MT, int NT, int CHUNK, bool LOCAL = false>
@@ -1265,6 +1369,19 @@ hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const int3
 {
     const int T = partial_tiles(N);
     const Window win{pos, grid_w, radius};
+    if (use_persistent(D, dt)) {
+        // The persistent kernel on the full schedule, one item per query block and its band.
+        const int cus = device_cus();
+        if (cus <= 0) return hipErrorInvalidDevice;
+        const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
+        if (dt == kBf16)
+            launch_persistent<Bf16, kPWC, kPWQ, kPMT, kPNT, false, true>(x, x_off, nullptr, B, N, D, T, xcds,
+                                                                         cus * kPWGS, pv, pi, stream, start, stop, win);
+        else
+            launch_persistent<F32, kPWC, kPWQ, kPMT, kPNT, false, true>(x, x_off, nullptr, B, N, D, T, xcds,
+                                                                        cus * kPWGS, pv, pi, stream, start, stop, win);
+        return hipGetLastError();
+    }
     if (dt == kBf16)
         return launch_staged<Bf16, 2, 4, 2, 2, 128, true>(x, x_off, B, N, D, T, pv, pi, stream, start, stop, win);
     return launch_staged<F32, 2, 2, 2, 2, 128, true>(x, x_off, B, N, D, T, pv, pi, stream, start, stop, win);

@@ -87,7 +87,11 @@ def test_window_hand_case_on_gpu(dtype):
 
 CASES = [  # (grid rows, grid cols, D, window, images)
     (5, 7, 64, 1, 3), (16, 16, 128, 2, 4), (17, 31, 96, 3, 2), (32, 32, 192, 0, 2), (20, 24, 64, 30, 2),
-    (40, 40, 256, 4, 3)]
+    (40, 40, 256, 4, 3),
+    # rows that are not a whole number of 64 bytes (bf16 80, f32 160): the register-staged kernel
+    (12, 9, 40, 2, 2),
+    # eight images or more: the persistent kernel's per-XCD image groups
+    (24, 24, 64, 3, 9)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
