@@ -119,7 +119,8 @@ def test_local_schedule_random_grids(dtype, gh, gw, D, window, B):
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("name,window,images", [("vit_b_512", 3, [0, 21, 63]), ("vit_l_1024", 4, [0, 9, 15])])
+@pytest.mark.parametrize("name,window,images", [("vit_b_512", 3, [0, 21, 63]), ("vit_l_1024", 4, [0, 9, 15]),
+                                                 ("stress_768", 4, [0, 5, 31])])
 def test_local_schedule_full_size(name, window, images):
     """The windowed schedule on a full benchmark batch (the launch configuration
     bench.py --window times), sampled images checked completely."""
