@@ -132,3 +132,47 @@ def test_local_schedule_full_size(name, window, images):
     flips = sum(check_local_schedule_image(x[b], cfg.dtype, res, b, cfg.G, window) for b in images)
     counts = [torch.diff(st.y_off.cpu()).tolist() for st in res.stages]
     print(f"  survivors (mean): {[round(sum(c) / len(c), 1) for c in counts]}, accepted flips {flips}", flush=True)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("given_pos", [False, True])
+def test_local_packed_edge_images(dtype, given_pos):
+    """One windowed insertion on packed ragged images: empty, one-token and two-token
+    images, images ending inside a grid row and inside a 256-token block, nine images
+    (the persistent kernel's per-XCD image groups), positions either each token's index
+    or a given increasing subset of the grid (every other cell, as after merges)."""
+    ns = [0, 1, 2, 37, 300, 513, 64, 256, 5]
+    grid_w, window, D = 19, 2, 64
+    rng = np.random.default_rng(11)
+    rows = [rng.standard_normal((n, D)) for n in ns]
+    x64 = [oracle.round_to(r, dtype) for r in rows]
+    off = np.concatenate([[0], np.cumsum(ns)]).astype(np.int32)
+    x = store(np.concatenate(x64), dtype).to(DEV)
+    poss = [2 * np.arange(n, dtype=np.int32) + 1 if given_pos else np.arange(n, dtype=np.int32) for n in ns]
+    pos = torch.from_numpy(np.concatenate(poss)).to(DEV) if given_pos else None
+    xo = torch.from_numpy(off).to(DEV)
+    print(f"local packed {dtype} given_pos={given_pos}: images {ns}", flush=True)
+    res = mpm.merge_local(x, grid_w, window, x_off=xo, N=max(ns), pos=pos)
+    torch.cuda.synchronize()
+    y_off = res.y_off.cpu().numpy()
+    for b, n in enumerate(ns):
+        cur, p = x64[b], poss[b]
+        nb = res.nb[b].cpu().numpy()[:n]
+        if n == 0:
+            assert y_off[b + 1] == y_off[b] and np.all(res.map[b].cpu().numpy() == -1), f"image {b}: empty"
+            continue
+        if n:
+            nn = oracle.nearest(cur, pos=p, grid_w=grid_w, window=window)
+            empty = nn.nb < 0
+            assert np.array_equal(nb[empty], nn.nb[empty]) and np.all(nb[~empty] >= 0), f"image {b}: empty windows"
+            gap = nn.top1 - nn.top2
+            for i in np.flatnonzero((nb != nn.nb) & ~empty):
+                sc = oracle.cosine(cur, int(i), int(nb[i]))
+                assert gap[i] < 1e-5 and sc >= nn.top1[i] - 1e-5, f"image {b} row {i}"
+        ref = oracle.merge(cur, dtype, nb=nb, pos=p, grid_w=grid_w, window=window)
+        m = res.map[b].cpu().numpy()
+        assert np.array_equal(m[:n], ref.map) and np.all(m[n:] == -1), f"image {b}: map"
+        assert y_off[b + 1] - y_off[b] == ref.count
+        y = to64(res.y[y_off[b]:y_off[b + 1]])
+        assert rel_err(y, ref.y) <= FEATURE_RTOL[dtype]
+        assert np.array_equal(res.y_pos[y_off[b]:y_off[b + 1]].cpu().numpy(), ref.y_pos), f"image {b}: positions"
