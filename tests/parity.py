@@ -48,7 +48,8 @@ def check_nearest(x64: np.ndarray, nb_gpu: np.ndarray, threads=None):
     """Returns (oracle Nearest, flipped_rows, near_tie_rows). Raises on a real mismatch."""
     n = x64.shape[0]
     nn = oracle.nearest(x64, threads)
-    gap = nn.top1 - nn.top2
+    with np.errstate(invalid="ignore"):  # rows without candidates: -inf - -inf (no near tie)
+        gap = nn.top1 - nn.top2
     near = int((gap < NEAR_TIE).sum()) if n > 1 else 0
     diff = np.nonzero(nb_gpu != nn.nb)[0]
     for i in diff:
