@@ -40,7 +40,8 @@ def check_local_schedule_image(x_img, dtype, res, b, grid_w, window, threads=Non
         idx = np.flatnonzero(~empty)
         if idx.size:
             # the near-tie check on rows with candidates: compare against the windowed top-1/2
-            gap = nn.top1 - nn.top2
+            with np.errstate(invalid="ignore"):
+                gap = nn.top1 - nn.top2
             for i in idx[nb[idx] != nn.nb[idx]]:
                 j = int(nb[i])
                 pi, pj = pos[i], pos[j]
