@@ -479,14 +479,13 @@ __host__ __device__ inline int deferred_diagonals(int nimg, int nb, int slots)
 // test, and writes one partial per query (tile slot 0, tile width N). Positions (win.pos,
 // null: the token's index) are fetched per tile while its K loop runs, as given norms are.
 //
-// xinv (may be null): the inverse row norms 1 / max(||x_j||, 1e-12), one float per row
-// packed like x, given instead of summed from the fragments in the K loop (vector ALU
-// work in the K loop adds to its time about one for one, and these sums are a tenth of
-// it). A run-time choice in one kernel, not a second build: the two insertions of a
-// schedule then run the same code, which a second build would evict from the
-// instruction cache at every switch (that cost 3-4% of the other insertion's launch).
+// GIVEN (bfloat16 rows only): xinv holds the inverse row norms 1 / max(||x_j||, 1e-12),
+// one float per row packed like x, which the kernel then takes instead of summing them
+// from the fragments in the K loop (vector ALU work in the K loop adds to its time about
+// one for one). Otherwise xinv is unused and every k-group's norm sums run without a
+// branch; each case is its own build.
 template <class S, int WC, int WQ, int MT, int NT, int CB, int STAGES, bool SYM, bool HALVES = false,
-          bool LOCAL = false>
+          bool LOCAL = false, bool GIVEN = false>
 __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  // 2 waves per SIMD
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, int B, int N, int D, int T, int xcds,
     int slots, float* __restrict__ pv, int32_t* __restrict__ pi, const float* __restrict__ xinv, Window win)
@@ -522,8 +521,8 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                   "window items: full schedule, square blocks, one position per thread");
     static_assert(!SYM || QT == CT, "the symmetric schedule pairs equal blocks");
     static_assert(CT + (SYM ? QT : 0) <= THREADS, "one given inverse norm per thread and item");
-    // Uniform. Bfloat16 rows only: the float32 kernels would spill a register with it.
-    const bool given = S::kBytes == 2 && xinv != nullptr;
+    static_assert(!GIVEN || S::kBytes == 2, "given norms: bfloat16 rows");
+    constexpr bool given = GIVEN;
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
@@ -731,10 +730,9 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     // Norm sums (rows not given): wave (wc, wq) sums candidate m-tiles wq, wq + WQ, ... and,
     // in the symmetric schedule, query n-tiles wc, wc + WC, ... It reads those fragments from
     // LDS a second time, before each k-group's MFMAs (own_c / own_q: their offsets in a stage,
-    // before the k column), and sums them after the MFMAs under one uniform branch per k-group.
-    // Picking them out of its registers by wave index instead took a branch per tile in the K
-    // loop, which cost 5-8% of the launch with norms summed. An index past the wave's tiles
-    // reads its last tile, whose sum is unused.
+    // before the k column), and sums them after the MFMAs. Picking them out of its registers
+    // by wave index instead took a branch per tile in the K loop, which cost 5-8% of the
+    // launch. An index past the wave's tiles reads its last tile, whose sum is unused.
     constexpr int NSC = (MT + WQ - 1) / WQ;
     constexpr int NSQ = SYM ? (NT + WC - 1) / WC : 1;
     float ss[NSC], sq[NSQ];
@@ -759,7 +757,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     constexpr int PPER = PSPAN >= LOADS ? 1 : (LOADS + PSPAN - 1) / PSPAN;  // loads per slot (small tiles)
     auto mma_issue = [&](const u32x4 (&fa)[MT], const u32x4 (&fq)[NT], int chunk, int g) {
         u32x4 oc[NSC], oq[NSQ];
-        {
+        if constexpr (!given) {
             const uint8_t* sb = lds + (chunk % STAGES) * STAGE_BYTES;
             const int col = ((2 * g + khalf) ^ sw) << 4;
 #pragma unroll
@@ -782,7 +780,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                 Mfma<S>::mma(acc[mt][nt], fa[mt], fq[nt]);
             }
         }
-        if (!given) {
+        if constexpr (!given) {
 #pragma unroll
             for (int j = 0; j < NSC; ++j) ss[j] = Mfma<S>::sumsq(oc[j], ss[j]);
             if constexpr (SYM) {
@@ -1223,8 +1221,8 @@ bool defers_diagonals(int B, int N, int xcds, int slots)
     return false;
 }
 
-template <class S, int WC, int WQ, int MT, int NT, bool SYM, bool LOCAL = false>
-void launch_persistent(const void* x, const int32_t* x_off, const float* xinv, int B, int N, int D, int T, int xcds,
+template <class S, int WC, int WQ, int MT, int NT, bool SYM, bool LOCAL, bool GIVEN>
+void launch_persistent_as(const void* x, const int32_t* x_off, const float* xinv, int B, int N, int D, int T, int xcds,
                        int groups, float* pv, int32_t* pi, hipStream_t stream, hipEvent_t start, hipEvent_t stop,
                        Window win = Window{nullptr, 1, 0})
 {
@@ -1233,19 +1231,38 @@ void launch_persistent(const void* x, const int32_t* x_off, const float* xinv, i
         // The symmetric schedule's deferred diagonal blocks, as half blocks, in a second launch
         // (one item per slot); the timing events then span both.
         const bool halves = SYM && defers_diagonals(B, N, xcds, groups / xcds);
-        hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB2, 2, SYM, false, LOCAL>), dim3(groups),
+        hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB2, 2, SYM, false, LOCAL, GIVEN>), dim3(groups),
                               dim3(WC * WQ * kWave), 0, stream, start, halves ? nullptr : stop, 0, xb, x_off, B, N,
                               D, T, xcds, groups / xcds, pv, pi, xinv, win);
         if constexpr (SYM) {
             if (halves)
-                hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT / 2, kPCB2, 2, false, true>),
+                hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT / 2, kPCB2, 2, false, true, false, GIVEN>),
                                       dim3(groups), dim3(WC * WQ * kWave), 0, stream, nullptr, stop, 0, xb, x_off, B,
                                       N, D, T, xcds, groups / xcds, pv, pi, xinv, win);
         }
     } else
-        hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB, 4, SYM, false, LOCAL>), dim3(groups),
+        hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB, 4, SYM, false, LOCAL, GIVEN>), dim3(groups),
                               dim3(WC * WQ * kWave), 0, stream, start, stop, 0, xb, x_off, B, N, D, T, xcds,
                               groups / xcds, pv, pi, xinv, win);
+}
+
+// Given norms (bfloat16 only) and norms summed in the K loop are separate builds: with one
+// build and a run-time flag, the flag's branch per k-group cost the summing launches 2-4%,
+// and two builds alternating between insertions showed no instruction-cache penalty.
+template <class S, int WC, int WQ, int MT, int NT, bool SYM, bool LOCAL = false>
+void launch_persistent(const void* x, const int32_t* x_off, const float* xinv, int B, int N, int D, int T, int xcds,
+                       int groups, float* pv, int32_t* pi, hipStream_t stream, hipEvent_t start, hipEvent_t stop,
+                       Window win = Window{nullptr, 1, 0})
+{
+    if constexpr (S::kBytes == 2) {
+        if (xinv != nullptr) {
+            launch_persistent_as<S, WC, WQ, MT, NT, SYM, LOCAL, true>(x, x_off, xinv, B, N, D, T, xcds, groups, pv,
+                                                                      pi, stream, start, stop, win);
+            return;
+        }
+    }
+    launch_persistent_as<S, WC, WQ, MT, NT, SYM, LOCAL, false>(x, x_off, nullptr, B, N, D, T, xcds, groups, pv, pi,
+                                                               stream, start, stop, win);
 }
 
 template <class S, int WC, int WQ, int MT, int NT, int CHUNK, bool LOCAL = false>
