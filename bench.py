@@ -33,9 +33,9 @@ METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak
 # rocprofv3 FETCH_SIZE / WRITE_SIZE runs on each workload, calibrated with a copy
 # kernel (profiles/<workload>_rocprof.md). Valid only for the kernel source it was
 # measured on, with the default schedule.
-TRAFFIC = {"source_sha256": "cf9f636df8205ea15bc9c82442f7420dd9359f824e84f6a0eb5de2ede72e9c12",
-           "bytes_per_launch": {"vit_ti_512": 6552821, "vit_s_512": 25843022, "vit_b_512": 151643237,
-                                "vit_l_1024": 510522497, "stress_768": 183317217}}
+TRAFFIC = {"source_sha256": "cc4f3b08e4dac54c1d8e21e1256da5a99d90f0423c6c67f23939c38c43f2e53d",
+           "bytes_per_launch": {"vit_ti_512": 6553836, "vit_s_512": 25826088, "vit_b_512": 151119932,
+                                "vit_l_1024": 511029509, "stress_768": 181739397}}
 
 
 def log(*a):
