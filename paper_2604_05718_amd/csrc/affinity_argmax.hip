@@ -517,8 +517,8 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     __shared__ int32_t red_ci[SYM ? WQ : 1][SYM ? CT : 1];
     // LOCAL: grid row [0] and column [1] of the item's candidates (0 .. CT-1) and queries (CT ..).
     __shared__ __attribute__((aligned(16))) int32_t win_rc[2][LOCAL ? CT + QT : 1];
-    static_assert(!LOCAL || (!SYM && !HALVES && QT == CT && CT + QT <= WC * WQ * kWave),
-                  "window items: full schedule, square blocks, one position per thread");
+    static_assert(!LOCAL || (!HALVES && QT == CT && CT + QT <= WC * WQ * kWave),
+                  "window items: square blocks, one position per thread");
     static_assert(!SYM || QT == CT, "the symmetric schedule pairs equal blocks");
     static_assert(CT + (SYM ? QT : 0) <= THREADS, "one given inverse norm per thread and item");
     static_assert(!GIVEN || S::kBytes == 2, "given norms: bfloat16 rows");
@@ -539,7 +539,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     const int per_img = LOCAL ? nqb : (SYM ? nqb * (nqb + 1) / 2 : nqb * nct);
     const int nimg = (B - group + xcds - 1) / xcds;
     static_assert(!HALVES || (!SYM && 2 * QT == CT), "half items: forward only, half a block of queries");
-    constexpr bool SPLIT = SYM && STAGES == 2;  // the layouts the second launch exists for
+    constexpr bool SPLIT = SYM && STAGES == 2 && !LOCAL;  // the layouts the second launch exists for
     const int ndef = (SPLIT || HALVES) ? deferred_diagonals(nimg, nct, slots) : 0;
     const int dfull = ndef / nct, dpart = ndef % nct;
     const int dimg = nimg - dfull - 1;                        // the image with dpart deferred
@@ -551,7 +551,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
     // Item cursor; all fields are uniform over the workgroup.
     struct Item {
         int k, b, qbase, cbase, n, row0;
-        int thi;  // LOCAL: the last candidate tile of the item's band (cbase walks up to it)
+        int tlo, thi;  // LOCAL: the item's band of candidate tiles (cbase walks up to thi)
     };
     auto find = [&](int k) {
         Item it;
@@ -605,6 +605,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
             const int n = x_off ? x_off[b + 1] - row0 : N;
             if (qbase < n && t * CT < n) {
                 it.k = k; it.b = b; it.qbase = qbase; it.cbase = t * CT; it.n = n; it.row0 = row0;
+                it.tlo = t;
                 it.thi = t;
                 if constexpr (LOCAL) {
                     // Candidate tiles whose grid rows can meet the block's window rows.
@@ -613,13 +614,16 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                     int tlo = 0, thi = (n - 1) / CT;
                     while (tlo < thi && grid_row(min((tlo + 1) * CT, n) - 1) < r_first - win.radius) ++tlo;
                     while (thi > tlo && grid_row(thi * CT) > r_last + win.radius) --thi;
-                    it.cbase = tlo * CT;
+                    // The symmetric schedule starts at the block's own tile: the tiles before
+                    // it reach this block through their own items' reverse direction.
+                    it.cbase = (SYM ? t : tlo) * CT;
+                    it.tlo = tlo;
                     it.thi = thi;
                 }
                 return it;
             }
         }
-        it.k = nitems; it.b = 0; it.qbase = 0; it.cbase = 0; it.n = 1; it.row0 = 0; it.thi = 0;
+        it.k = nitems; it.b = 0; it.qbase = 0; it.cbase = 0; it.n = 1; it.row0 = 0; it.tlo = 0; it.thi = 0;
         return it;
     };
     // The work after `it`: its next band tile (LOCAL), else the slot's next item.
@@ -944,6 +948,26 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
         const uint32_t wspan = 2u * (uint32_t)win.radius;
         // This lane's own row inside a 32-row tile, as an accumulator element (if it holds it).
         const int self_r = (((lrow >> 2) & 1) == khalf) ? 4 * (lrow >> 3) + (lrow & 3) : -1;
+        if constexpr (LOCAL && SYM) {
+            // Both directions read the accumulators: pairs outside the window become -inf
+            // there (the inverse norms that scale them are positive).
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int jl = wc * MT * 32 + mt * 32 + 8 * g + 4 * khalf;
+                    const int4 cr = *reinterpret_cast<const int4*>(&win_rc[0][jl]);
+                    const int4 cc = *reinterpret_cast<const int4*>(&win_rc[1][jl]);
+                    const int crv[4] = {cr.x, cr.y, cr.z, cr.w}, ccv[4] = {cc.x, cc.y, cc.z, cc.w};
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const bool in = (uint32_t)(crv[e] - q_r[nt]) <= wspan && (uint32_t)(ccv[e] - q_c[nt]) <= wspan;
+                            acc[mt][nt][4 * g + e] = in ? acc[mt][nt][4 * g + e] : -__builtin_inff();
+                        }
+                }
+        }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             if (mt >= mt_lim) break;
@@ -970,7 +994,7 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
 #pragma unroll
                     for (int r = 0; r < 16; ++r) sc[r] = r == self_r ? -__builtin_inff() : sc[r];
                 }
-                if constexpr (LOCAL) {
+                if constexpr (LOCAL && !SYM) {
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
                         const int jl = wc * MT * 32 + mt * 32 + 8 * g + 4 * khalf;
@@ -1129,8 +1153,12 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                     red_i[wc][ql] = i;
                 }
             }
-            lds_barrier();
-            const int t = LOCAL ? 0 : cb / CT;  // LOCAL: one partial per query, tile slot 0
+        }
+        if (item_end || rev) lds_barrier();  // uniform
+        if (item_end) {
+            // The query block's partial: tile slot t (LOCAL: slot 0, or the block's own slot
+            // under the symmetric schedule, whose earlier slots take the reverse direction).
+            const int t = LOCAL ? (SYM ? ci.qbase / QT : 0) : cb / CT;
             for (int ql = tid; ql < QT; ql += THREADS) {
                 const int qi = ci.qbase + ql;
                 if (qi >= n) continue;
@@ -1148,21 +1176,35 @@ __global__ __launch_bounds__(WC * WQ * kWave, 2) void affinity_partial_kernel(  
                 const long o = ((long)ci.b * T + t) * N + qi;
                 pv[o] = v;
                 pi[o] = i;
-            }
-            if (rev) {
-                // Candidate rows of the tile over the query block: tile slot qbase / QT of their partials.
-                const int tq = ci.qbase / QT;
-                for (int jl = tid; jl < CT; jl += THREADS) {
-                    const int j = cb + jl;
-                    if (j >= n) continue;
-                    float v = red_cv[0][jl];
-                    int32_t i = red_ci[0][jl];
-#pragma unroll
-                    for (int w = 1; w < WQ; ++w) merge_pair(v, i, v, i, red_cv[w][jl], red_ci[w][jl]);
-                    const long o = ((long)ci.b * T + tq) * N + j;
-                    pv[o] = v;
-                    pi[o] = i;
+                if constexpr (LOCAL && SYM) {
+                    // The slots no item writes for this block's rows: tiles before the band and
+                    // after the block (the band relation is symmetric, so the items that write
+                    // slot q for these rows are exactly the blocks q of the band before it).
+                    const int nq = (n + QT - 1) / QT;
+                    for (int q = 0; q < nq; ++q) {
+                        if (q >= ci.tlo && q <= t) continue;
+                        const long oq = ((long)ci.b * T + q) * N + qi;
+                        pv[oq] = -__builtin_inff();
+                        pi[oq] = -1;
+                    }
                 }
+            }
+        }
+        if (rev) {
+            // Candidate rows of the tile over the query block: tile slot qbase / QT of their partials.
+            const int tq = ci.qbase / QT;
+            for (int jl = tid; jl < CT; jl += THREADS) {
+                const int j = cb + jl;
+                if (j >= n) continue;
+                float v = red_cv[0][jl];
+                int32_t i = red_ci[0][jl];
+#pragma unroll
+                for (int w = 1; w < WQ; ++w) merge_pair(v, i, v, i, red_cv[w][jl], red_ci[w][jl]);
+                // A row with no query of the block inside its window: -inf, and no index.
+                if (LOCAL && v == -__builtin_inff()) i = -1;
+                const long o = ((long)ci.b * T + tq) * N + j;
+                pv[o] = v;
+                pi[o] = i;
             }
         }
         cchunk = 0;
@@ -1230,7 +1272,7 @@ void launch_persistent_as(const void* x, const int32_t* x_off, const float* xinv
     if (((long)D * S::kBytes) % kPCB2 == 0) {
         // The symmetric schedule's deferred diagonal blocks, as half blocks, in a second launch
         // (one item per slot); the timing events then span both.
-        const bool halves = SYM && defers_diagonals(B, N, xcds, groups / xcds);
+        const bool halves = SYM && !LOCAL && defers_diagonals(B, N, xcds, groups / xcds);
         hipExtLaunchKernelGGL((affinity_partial_kernel<S, WC, WQ, MT, NT, kPCB2, 2, SYM, false, LOCAL, GIVEN>), dim3(groups),
                               dim3(WC * WQ * kWave), 0, stream, start, halves ? nullptr : stop, 0, xb, x_off, B, N,
                               D, T, xcds, groups / xcds, pv, pi, xinv, win);
@@ -1316,6 +1358,8 @@ bool symmetric_schedule(int B, int N, int xcds, int slots, int schedule)
 
 }  // namespace
 
+int local_partial_tile_width(int D, int dt, int N) { return use_persistent(D, dt) ? kPCT : N; }
+
 int partial_tile_width(int B, int D, int dt, int N, int schedule)
 {
     if (!use_persistent(D, dt)) return N;
@@ -1387,16 +1431,17 @@ hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const int3
     const int T = partial_tiles(N);
     const Window win{pos, grid_w, radius};
     if (use_persistent(D, dt)) {
-        // The persistent kernel on the full schedule, one item per query block and its band.
+        // The persistent kernel on the symmetric schedule, one item per query block and the
+        // tiles of its band from its own on.
         const int cus = device_cus();
         if (cus <= 0) return hipErrorInvalidDevice;
         const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
         if (dt == kBf16)
-            launch_persistent<Bf16, kPWC, kPWQ, kPMT, kPNT, false, true>(x, x_off, nullptr, B, N, D, T, xcds,
-                                                                         cus * kPWGS, pv, pi, stream, start, stop, win);
-        else
-            launch_persistent<F32, kPWC, kPWQ, kPMT, kPNT, false, true>(x, x_off, nullptr, B, N, D, T, xcds,
+            launch_persistent<Bf16, kSWC, kSWQ, kSMT, kSNT, true, true>(x, x_off, nullptr, B, N, D, T, xcds,
                                                                         cus * kPWGS, pv, pi, stream, start, stop, win);
+        else
+            launch_persistent<F32, kSWC, kSWQ, kSMT, kSNT, true, true>(x, x_off, nullptr, B, N, D, T, xcds,
+                                                                       cus * kPWGS, pv, pi, stream, start, stop, win);
         return hipGetLastError();
     }
     if (dt == kBf16)

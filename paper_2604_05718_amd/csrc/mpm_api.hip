@@ -140,17 +140,24 @@ constexpr int kFusedReduceMaxTiles = 4;
 constexpr int kFusedReduceMaxTilesFewImages = 16;
 constexpr int kFewImages = 8;
 
-hipError_t compact_from_partials(const Workspace& w, const int32_t* x_off, int32_t B, int32_t N, int32_t D,
-                                 int32_t dt, int32_t schedule, int32_t* map, int32_t* y_off, hipStream_t st)
+// Compaction from partials of ct candidate rows each (reduced first by their own launch
+// when an image has more tiles than the compaction reduces well itself).
+hipError_t compact_partials_ct(const Workspace& w, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt,
+                               int ct, int32_t* map, int32_t* y_off, hipStream_t st)
 {
     const int T = mpm::partial_tiles(N);
-    const int ct = mpm::partial_tile_width(B, D, dt, N, schedule);
     const int fused_max = B <= kFewImages ? kFusedReduceMaxTilesFewImages : kFusedReduceMaxTiles;
     if ((N + ct - 1) / ct <= fused_max)
         return mpm::launch_pair_compact_partials(w.pv, w.pi, T, ct, w.nb, x_off, B, N, map, w.src, y_off, w.sync, st);
     hipError_t e = mpm::launch_reduce_partials(w.pv, w.pi, ct, nullptr, x_off, B, N, D, dt, w.nb, nullptr, st);
     if (e == hipSuccess) e = mpm::launch_pair_compact(w.nb, x_off, B, N, map, w.src, y_off, w.sync, st);
     return e;
+}
+
+hipError_t compact_from_partials(const Workspace& w, const int32_t* x_off, int32_t B, int32_t N, int32_t D,
+                                 int32_t dt, int32_t schedule, int32_t* map, int32_t* y_off, hipStream_t st)
+{
+    return compact_partials_ct(w, x_off, B, N, D, dt, mpm::partial_tile_width(B, D, dt, N, schedule), map, y_off, st);
 }
 
 // One insertion's affinity (events bound to its launches) and compaction into the carved workspace.
@@ -377,13 +384,11 @@ int mpm_merge_local(const void* x, const int32_t* x_off, const int32_t* pos, int
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     MPM_LAUNCH_GATE();
     const hipStream_t st = as_stream(stream);
-    // One partial per token (the kernel covers every candidate tile of the window itself).
     hipError_t e = mpm::launch_affinity_local(x, x_off, pos, grid_w, window, B, N, D, dt, w.pv, w.pi, st,
                                               static_cast<hipEvent_t>(start_event),
                                               static_cast<hipEvent_t>(stop_event));
     if (e == hipSuccess)
-        e = mpm::launch_pair_compact_partials(w.pv, w.pi, mpm::partial_tiles(N), N, w.nb, x_off, B, N, map, w.src,
-                                              y_off, w.sync, st);
+        e = compact_partials_ct(w, x_off, B, N, D, dt, mpm::local_partial_tile_width(D, dt, N), map, y_off, st);
     if (e == hipSuccess)
         e = mpm::launch_pair_average(x, x_off, w.src, y_off, B, N, D, dt, y, nullptr, st, pos, y_pos);
     return hip_status(e);
