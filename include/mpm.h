@@ -273,6 +273,8 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
  * quadratic affinity that the paper proposes (Sec. 5, also Sec. 4.3). A token's
  * position is its raster index on a grid of grid_w columns (row = pos / grid_w,
  * column = pos % grid_w):
+ *   x_inv (may be NULL): given inverse norms of the rows of x, as in mpm_affinity;
+ *   y_inv (may be NULL): inverse norms of the merged rows, as in mpm_pair_average;
  *   pos (may be NULL): int32 per row of x, packed like x; NULL means each token's
  *       index in its image (the raster order of a full grid, as for a first
  *       insertion); positions must be non-decreasing in row along each image;
@@ -283,6 +285,7 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
  *   y_pos[y_off[b] + k] = the position of cluster k's representative (int32, packed
  *       like y): the pos of the merged rows for the next insertion, which keeps the
  *       raster order since ids follow the left-to-right scan.
+ * Feed (y, y_off, y_inv, y_pos) as (x, x_off, x_inv, pos) of the next insertion.
  * Only the candidate tiles a query block's window reaches are computed. The
  * workspace as in mpm_merge (nb and src readable after the call). start_event /
  * stop_event (may be NULL) are bound to the affinity kernel's dispatch, as in
@@ -290,9 +293,10 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
  * mpm_merge, plus MPM_ERR_INVALID_ARG for grid_w < 1, grid_w > MPM_MAX_N or
  * window < 0. Positions outside [0, grid_w * MPM_MAX_N) are undefined behaviour.
  */
-int mpm_merge_local(const void* x, const int32_t* x_off, const int32_t* pos, int32_t B, int32_t N, int32_t D,
-                    int32_t dt, int32_t grid_w, int32_t window, void* y, int32_t* y_off, int32_t* y_pos, int32_t* map,
-                    void* ws, size_t ws_bytes, void* start_event, void* stop_event, void* stream);
+int mpm_merge_local(const void* x, const int32_t* x_off, const float* x_inv, const int32_t* pos, int32_t B,
+                    int32_t N, int32_t D, int32_t dt, int32_t grid_w, int32_t window, void* y, int32_t* y_off,
+                    float* y_inv, int32_t* y_pos, int32_t* map, void* ws, size_t ws_bytes, void* start_event,
+                    void* stop_event, void* stream);
 
 /*
  * Padded batch layout (the paper pads each batch to its longest image, Sec. 4.2): the

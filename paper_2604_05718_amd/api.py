@@ -220,11 +220,12 @@ def insertion(x, x_off=None, N=None, x_inv=None, want_inv=False, ws=None, schedu
     return Merged(y, y_off, m, ws, B, N, y_inv)
 
 
-def merge_local(x, grid_w: int, window: int, x_off=None, N=None, pos=None, ws=None) -> Merged:
+def merge_local(x, grid_w: int, window: int, x_off=None, N=None, pos=None, ws=None, x_inv=None,
+                want_inv=False) -> Merged:
     """One locality-constrained insertion (Sec. 5): candidates within ``window`` rows and
     columns on a grid of ``grid_w`` columns; ``pos`` the tokens' raster positions
     (packed like x; None: each token's index in its image). The merged rows'
-    positions are returned in ``y_pos``."""
+    positions are returned in ``y_pos``; ``x_inv`` / ``want_inv`` as in merge()."""
     x2, B, N, D = _rows(x, N, x_off)
     dev = x.device
     ws = _workspace(B, N, dev, ws)
@@ -232,10 +233,12 @@ def merge_local(x, grid_w: int, window: int, x_off=None, N=None, pos=None, ws=No
     y_off = torch.empty((B + 1,), dtype=torch.int32, device=dev)
     y_pos = torch.empty((B * N,), dtype=torch.int32, device=dev)
     m = torch.empty((B, N), dtype=torch.int32, device=dev)
-    _lib.check("mpm_merge_local", _lib.load().mpm_merge_local(_p(x2), _p(x_off), _p(pos), B, N, D, _dt(x), int(grid_w),
-                                                              int(window), _p(y), _p(y_off), _p(y_pos), _p(m), _p(ws),
-                                                              ws.numel(), None, None, _stream()))
-    return Merged(y, y_off, m, ws, B, N, None, y_pos)
+    y_inv = torch.empty((B * N,), dtype=torch.float32, device=dev) if want_inv else None
+    _lib.check("mpm_merge_local", _lib.load().mpm_merge_local(_p(x2), _p(x_off), _p(x_inv), _p(pos), B, N, D, _dt(x),
+                                                              int(grid_w), int(window), _p(y), _p(y_off), _p(y_inv),
+                                                              _p(y_pos), _p(m), _p(ws), ws.numel(), None, None,
+                                                              _stream()))
+    return Merged(y, y_off, m, ws, B, N, y_inv, y_pos)
 
 
 def pad(z, z_off, P: int, out=None):
@@ -321,14 +324,15 @@ def run_schedule(x, insertions: int = 2, workspaces=None, schedule: str = "auto"
     ``window``, every insertion is locality-constrained (merge_local) on a grid of
     ``grid_w`` columns, the first on the raster positions."""
     B, N, D = x.shape
-    norms = takes_norms(D, x.dtype) and window is None
+    norms = takes_norms(D, x.dtype)
     stages = []
     cur, cur_off, cur_inv, cur_pos = x, None, None, None
     rstar = None
     for s in range(insertions):
         ws = None if workspaces is None else workspaces[s]
         if window is not None:
-            m = merge_local(cur, grid_w, window, x_off=cur_off, N=N, pos=cur_pos, ws=ws)
+            m = merge_local(cur, grid_w, window, x_off=cur_off, N=N, pos=cur_pos, ws=ws, x_inv=cur_inv,
+                            want_inv=norms and s + 1 < insertions)
         else:
             m = merge(cur, cur_off, N=N, x_inv=cur_inv, want_inv=norms and s + 1 < insertions, ws=ws,
                       schedule=schedule)
@@ -374,7 +378,7 @@ class Schedule:
         self.y = [torch.empty((B * N, D), dtype=dtype, device=dev) for _ in range(insertions)]
         self.y_off = [torch.empty((B + 1,), **i32) for _ in range(insertions)]
         # Inverse norms of each insertion's merged rows, for the next insertion's affinity.
-        norms = takes_norms(D, dtype) and window is None
+        norms = takes_norms(D, dtype)
         self.y_inv = [torch.empty((B * N,), dtype=torch.float32, device=dev) if norms and s + 1 < insertions
                       else None for s in range(insertions)]
         self.y_pos = [torch.empty((B * N,), **i32) if window is not None else None for _ in range(insertions)]
@@ -418,9 +422,10 @@ class Schedule:
             if self.window is not None:
                 ev0, ev1 = (None, None) if affinity_events is None else (c_event(e) for e in affinity_events[s])
                 _lib.check("mpm_merge_local", lib.mpm_merge_local(
-                    _p(cur), _p(cur_off), _p(cur_pos), B, N, D, dt, self.grid_w, self.window, _p(self.y[s]),
-                    _p(self.y_off[s]), _p(self.y_pos[s]), _p(self.map[s]), _p(ws), ws.numel(), ev0, ev1, st))
-                cur, cur_off, cur_pos = self.y[s], self.y_off[s], self.y_pos[s]
+                    _p(cur), _p(cur_off), _p(cur_inv), _p(cur_pos), B, N, D, dt, self.grid_w, self.window,
+                    _p(self.y[s]), _p(self.y_off[s]), _p(self.y_inv[s]), _p(self.y_pos[s]), _p(self.map[s]), _p(ws),
+                    ws.numel(), ev0, ev1, st))
+                cur, cur_off, cur_inv, cur_pos = self.y[s], self.y_off[s], self.y_inv[s], self.y_pos[s]
                 continue
             ev0, ev1 = (None, None) if affinity_events is None else (c_event(e) for e in affinity_events[s])
             _lib.check("mpm_affinity_compact", lib.mpm_affinity_compact(

@@ -1424,7 +1424,8 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
     return launch_staged<F32, 2, 2, 2, 2, 128>(x, x_off, B, N, D, T, pv, pi, stream, start, stop);
 }
 
-hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const int32_t* pos, int grid_w, int radius,
+hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const float* xinv, const int32_t* pos,
+                                 int grid_w, int radius,
                                  int B, int N, int D, int dt, float* pv, int32_t* pi, hipStream_t stream,
                                  hipEvent_t start, hipEvent_t stop)
 {
@@ -1432,12 +1433,12 @@ hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const int3
     const Window win{pos, grid_w, radius};
     if (use_persistent(D, dt)) {
         // The persistent kernel on the symmetric schedule, one item per query block and the
-        // tiles of its band from its own on.
+        // tiles of its band from its own on (given norms: bf16 only).
         const int cus = device_cus();
         if (cus <= 0) return hipErrorInvalidDevice;
         const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
         if (dt == kBf16)
-            launch_persistent<Bf16, kSWC, kSWQ, kSMT, kSNT, true, true>(x, x_off, nullptr, B, N, D, T, xcds,
+            launch_persistent<Bf16, kSWC, kSWQ, kSMT, kSNT, true, true>(x, x_off, xinv, B, N, D, T, xcds,
                                                                         cus * kPWGS, pv, pi, stream, start, stop, win);
         else
             launch_persistent<F32, kSWC, kSWQ, kSMT, kSNT, true, true>(x, x_off, nullptr, B, N, D, T, xcds,

@@ -371,26 +371,28 @@ int mpm_merge_noalloc(const void* x, const int32_t* x_off, const float* x_inv, i
     return hip_status(e);
 }
 
-int mpm_merge_local(const void* x, const int32_t* x_off, const int32_t* pos, int32_t B, int32_t N, int32_t D,
-                    int32_t dt, int32_t grid_w, int32_t window, void* y, int32_t* y_off, int32_t* y_pos, int32_t* map,
-                    void* ws, size_t ws_bytes, void* start_event, void* stop_event, void* stream)
+int mpm_merge_local(const void* x, const int32_t* x_off, const float* x_inv, const int32_t* pos, int32_t B,
+                    int32_t N, int32_t D, int32_t dt, int32_t grid_w, int32_t window, void* y, int32_t* y_off,
+                    float* y_inv, int32_t* y_pos, int32_t* map, void* ws, size_t ws_bytes, void* start_event,
+                    void* stop_event, void* stream)
 {
-    int s = check_affinity(x, x_off, nullptr, B, N, D, dt, MPM_SCHEDULE_AUTO);
+    int s = check_affinity(x, x_off, x_inv, B, N, D, dt, MPM_SCHEDULE_AUTO);
     if (s != MPM_OK) return s;
-    if (!ok_opt_int_ptr(pos) || !ok_rows_ptr(y) || !ok_int_ptr(y_off) || !ok_int_ptr(y_pos) || !ok_int_ptr(map))
+    if (!ok_opt_int_ptr(pos) || !ok_rows_ptr(y) || !ok_int_ptr(y_off) || !ok_opt_int_ptr(y_inv) ||
+        !ok_int_ptr(y_pos) || !ok_int_ptr(map))
         return MPM_ERR_INVALID_ARG;
     if (grid_w < 1 || grid_w > MPM_MAX_N || window < 0) return MPM_ERR_INVALID_ARG;
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     MPM_LAUNCH_GATE();
     const hipStream_t st = as_stream(stream);
-    hipError_t e = mpm::launch_affinity_local(x, x_off, pos, grid_w, window, B, N, D, dt, w.pv, w.pi, st,
+    hipError_t e = mpm::launch_affinity_local(x, x_off, x_inv, pos, grid_w, window, B, N, D, dt, w.pv, w.pi, st,
                                               static_cast<hipEvent_t>(start_event),
                                               static_cast<hipEvent_t>(stop_event));
     if (e == hipSuccess)
         e = compact_partials_ct(w, x_off, B, N, D, dt, mpm::local_partial_tile_width(D, dt, N), map, y_off, st);
     if (e == hipSuccess)
-        e = mpm::launch_pair_average(x, x_off, w.src, y_off, B, N, D, dt, y, nullptr, st, pos, y_pos);
+        e = mpm::launch_pair_average(x, x_off, w.src, y_off, B, N, D, dt, y, y_inv, st, pos, y_pos);
     return hip_status(e);
 }
 

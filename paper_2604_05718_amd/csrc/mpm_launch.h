@@ -47,17 +47,19 @@ hipError_t launch_pair_compact(const int32_t* nb, const int32_t* x_off, int B, i
 hipError_t launch_zero_words(int32_t* p, long words, hipStream_t stream);
 
 // y_inv (may be null) receives 1 / max(||y_k||, 1e-12) of every merged row k, packed like y.
-// y_pos (may be null; not with y_inv) receives each merged row's grid position: its
+// y_pos (may be null) receives each merged row's grid position: its
 // representative's pos (packed like x; null: its index in the image).
 hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_t* src, const int32_t* y_off, int B,
                                int N, int D, int dt, void* y, float* y_inv, hipStream_t stream,
                                const int32_t* pos = nullptr, int32_t* y_pos = nullptr);
 // The affinity partials under the locality constraint (Sec. 5): candidates of each token
 // restricted to the cells within `radius` rows and columns of its own on a grid of
-// grid_w columns (pos: raster positions packed like x, or null for each token's index);
-// partials of local_partial_tile_width(D, dt, N) candidate rows each, every slot of an
-// image's tiles written (-inf, -1 where the window reaches no candidate of a tile).
-hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const int32_t* pos, int grid_w, int radius,
+// grid_w columns (pos: raster positions packed like x, or null for each token's index;
+// xinv: given inverse norms, or null to sum them); partials of
+// local_partial_tile_width(D, dt, N) candidate rows each, every slot of an image's tiles
+// written (-inf, -1 where the window reaches no candidate of a tile).
+hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const float* xinv, const int32_t* pos,
+                                 int grid_w, int radius,
                                  int B, int N, int D, int dt, float* pv, int32_t* pi, hipStream_t stream,
                                  hipEvent_t start, hipEvent_t stop);
 

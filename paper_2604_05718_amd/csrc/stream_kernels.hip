@@ -150,12 +150,13 @@ __global__ __launch_bounds__(kRowThreads) void pair_average_kernel(
 // stored values. A group of G = inv_lanes(vpr) lanes takes a row: lane j its vectors
 // j, j + G, ..., kInvBatch at a time (all loaded before any is stored), summing their
 // squares in that order; a butterfly across the group adds the lanes' sums. The order
-// is fixed, so the result is the same on every run. The merged rows are those of
-// pair_average_kernel, bit for bit.
+// is fixed, so the result is the same on every run. The merged rows (and positions) are
+// those of pair_average_kernel, bit for bit.
 template <class S>
 __global__ __launch_bounds__(kRowThreads) void pair_average_inv_kernel(
     const uint8_t* __restrict__ x, const int32_t* __restrict__ x_off, const int32_t* __restrict__ src,
-    const int32_t* __restrict__ y_off, int N, int D, uint8_t* __restrict__ y, float* __restrict__ y_inv)
+    const int32_t* __restrict__ y_off, int N, int D, uint8_t* __restrict__ y, float* __restrict__ y_inv,
+    const int32_t* __restrict__ pos, int32_t* __restrict__ y_pos)
 {
     const int b = blockIdx.y;
     const Span sp = output_span(y_off, b, N, gridDim.y);
@@ -200,7 +201,10 @@ __global__ __launch_bounds__(kRowThreads) void pair_average_inv_kernel(
         }
     }
     for (int o = G / 2; o > 0; o >>= 1) t += __shfl_xor(t, o);
-    if (live && j == 0) y_inv[off + k] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+    if (live && j == 0) {
+        y_inv[off + k] = 1.0f / fmaxf(sqrtf(t), 1e-12f);
+        if (y_pos) y_pos[off + k] = pos ? pos[(x_off ? x_off[b] : b * N) + ia] : ia;  // the representative's
+    }
 }
 
 __global__ __launch_bounds__(kRowThreads) void compose_kernel(const int32_t* map_a,
@@ -313,15 +317,15 @@ hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_
     dim3 grid((N + rpb - 1) / rpb, B);
     const uint8_t* xp = static_cast<const uint8_t*>(x);
     uint8_t* yp = static_cast<uint8_t*>(y);
-    if (y_inv && !y_pos) {
+    if (y_inv) {
         const int rows = kRowThreads / inv_lanes((int)(rowbytes / 16));
         const dim3 igrid((N + rows - 1) / rows, B);
         if (dt == kBf16)
             hipLaunchKernelGGL(pair_average_inv_kernel<Bf16>, igrid, dim3(kRowThreads), 0, stream, xp, x_off, src,
-                               y_off, N, D, yp, y_inv);
+                               y_off, N, D, yp, y_inv, pos, y_pos);
         else
             hipLaunchKernelGGL(pair_average_inv_kernel<F32>, igrid, dim3(kRowThreads), 0, stream, xp, x_off, src,
-                               y_off, N, D, yp, y_inv);
+                               y_off, N, D, yp, y_inv, pos, y_pos);
         return hipGetLastError();
     }
     if (dt == kBf16)

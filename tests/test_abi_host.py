@@ -130,7 +130,8 @@ def test_other_entry_points_reject(lib):
 def test_pad_unpad_and_local_reject(lib):
     """mpm_pad / mpm_unpad and mpm_merge_local return their argument errors before any
     device work: sizes, row bytes that are not whole 16-byte vectors, NULL or misaligned
-    pointers, a grid or window the locality constraint cannot take, a short workspace."""
+    pointers, a grid or window the locality constraint cannot take, a short workspace,
+    given norms for rows the norm-taking kernel does not cover."""
     for fn in (lib.mpm_pad, lib.mpm_unpad):
         assert fn(A, A, 0, 8, 64, A2, None) == 1             # B < 1
         assert fn(A, A, 2, 0, 64, A2, None) == 1             # P < 1
@@ -147,15 +148,20 @@ def test_pad_unpad_and_local_reject(lib):
 
     def local(**kw):
         a = dict(ok, **kw)
-        return lib.mpm_merge_local(A, None, a["pos"], 2, 64, 64, 1, a["grid_w"], a["window"], A2, A2, a["y_pos"],
-                                   A2, A2, a.get("ws", ws), None, None, None)
+        return lib.mpm_merge_local(A, None, a.get("x_inv"), a["pos"], 2, 64, a.get("D", 64), a.get("dt", 1),
+                                   a["grid_w"], a["window"], A2, A2, a.get("y_inv"), a["y_pos"], A2, A2,
+                                   a.get("ws", ws), None, None, None)
     assert local(grid_w=0) == 1
     assert local(grid_w=16385) == 1
     assert local(window=-1) == 1
     assert local(y_pos=None) == 1
     assert local(pos=odd) == 1                                # positions misaligned
     assert local(ws=16) == 3                                  # workspace too small
-    assert lib.mpm_merge_local(A, None, None, 2, 64, 63, 1, 8, 1, A2, A2, A2, A2, A2, ws, None, None, None) == 1
+    assert local(D=63) == 1                                   # D % 8 (bf16)
+    assert local(x_inv=odd) == 1                              # given norms misaligned
+    assert local(y_inv=odd) == 1
+    assert local(x_inv=A, D=40) == 2                          # given norms: 80-byte rows
+    assert local(x_inv=A, dt=0) == 2                          # given norms: float32 rows
     assert lib.mpm_last_hip_error() == 0
 
 

@@ -135,13 +135,15 @@ def test_local_schedule_full_size(name, window, images):
     print(f"  survivors (mean): {[round(sum(c) / len(c), 1) for c in counts]}, accepted flips {flips}", flush=True)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dtype,given_norms", [("f32", False), ("bf16", False), ("bf16", True)])
 @pytest.mark.parametrize("given_pos", [False, True])
-def test_local_packed_edge_images(dtype, given_pos):
+def test_local_packed_edge_images(dtype, given_norms, given_pos):
     """One windowed insertion on packed ragged images: empty, one-token and two-token
     images, images ending inside a grid row and inside a 256-token block, nine images
     (the persistent kernel's per-XCD image groups), positions either each token's index
-    or a given increasing subset of the grid (every other cell, as after merges)."""
+    or a given increasing subset of the grid (every other cell, as after merges); the
+    inverse norms either summed by the kernel or given (float64-exact, rounded to
+    float32), and those of the merged rows written."""
     ns = [0, 1, 2, 37, 300, 513, 64, 256, 5]
     grid_w, window, D = 19, 2, 64
     rng = np.random.default_rng(11)
@@ -152,8 +154,12 @@ def test_local_packed_edge_images(dtype, given_pos):
     poss = [2 * np.arange(n, dtype=np.int32) + 1 if given_pos else np.arange(n, dtype=np.int32) for n in ns]
     pos = torch.from_numpy(np.concatenate(poss)).to(DEV) if given_pos else None
     xo = torch.from_numpy(off).to(DEV)
-    print(f"local packed {dtype} given_pos={given_pos}: images {ns}", flush=True)
-    res = mpm.merge_local(x, grid_w, window, x_off=xo, N=max(ns), pos=pos)
+    x_inv = None
+    if given_norms:
+        inv = np.concatenate([1.0 / np.maximum(np.sqrt((r ** 2).sum(axis=1)), 1e-12) for r in x64])
+        x_inv = torch.from_numpy(inv.astype(np.float32)).to(DEV)
+    print(f"local packed {dtype} given_norms={given_norms} given_pos={given_pos}: images {ns}", flush=True)
+    res = mpm.merge_local(x, grid_w, window, x_off=xo, N=max(ns), pos=pos, x_inv=x_inv, want_inv=True)
     torch.cuda.synchronize()
     y_off = res.y_off.cpu().numpy()
     for b, n in enumerate(ns):
@@ -178,3 +184,7 @@ def test_local_packed_edge_images(dtype, given_pos):
         y = to64(res.y[y_off[b]:y_off[b + 1]])
         assert rel_err(y, ref.y) <= FEATURE_RTOL[dtype]
         assert np.array_equal(res.y_pos[y_off[b]:y_off[b + 1]].cpu().numpy(), ref.y_pos), f"image {b}: positions"
+        # the merged rows' inverse norms, from their stored values (float32 sums)
+        yi = res.y_inv[y_off[b]:y_off[b + 1]].cpu().numpy().astype(np.float64)
+        want = 1.0 / np.maximum(np.sqrt((y ** 2).sum(axis=1)), 1e-12)
+        assert np.max(np.abs(yi / want - 1.0)) <= 1e-5, f"image {b}: merged inverse norms"
