@@ -53,6 +53,19 @@
  *   at the first call), every entry point that would launch a kernel returns
  *   MPM_ERR_HIP with hipErrorLaunchFailure recorded, after its argument checks and
  *   before any HIP call, so that callers' error paths can be tested without a GPU.
+ * - Checked mode (debugging): with MPM_CHECKED=1 in the environment (read once, at
+ *   the first call), every entry point also validates on the device the data
+ *   preconditions that are otherwise undefined behaviour, before launching its
+ *   operation: packed offsets (1 <= n_b <= N; merged-row offsets also at most the
+ *   tokens they come from, within B*N rows; the padded layout's at most P), token
+ *   values and given inverse norms (finite; norms positive), grid positions (in
+ *   range, rows non-decreasing), neighbours (in [0, n_b), not the token itself, -1
+ *   for a one-token image), merged-row sources (in [0, n_b)) and maps (in [-1, N),
+ *   or [-1, n_z) where they index merged rows). Offsets are validated first; the
+ *   rows they address must exist. On a violation the call returns
+ *   MPM_ERR_INVALID_ARG and launches nothing of its operation. A checked call
+ *   synchronises its stream (it reads the verdict back), and checked calls are
+ *   serialised by a lock. Without the variable nothing of this runs.
  */
 #ifndef MPM_H
 #define MPM_H

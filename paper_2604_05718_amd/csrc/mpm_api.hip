@@ -46,6 +46,124 @@ int injected_failure() { return hip_status(hipErrorLaunchFailure); }
         if (inject_launch_failure()) return injected_failure();    \
     } while (0)
 
+// Checked mode: with MPM_CHECKED=1 in the environment (read once, at the first call),
+// every entry point validates the data-dependent preconditions it would otherwise take
+// on trust, on the device, before launching its operation: packed offsets first (their
+// verdict read back), then the values the operation indexes with. A failure returns
+// MPM_ERR_INVALID_ARG with nothing of the operation launched. The verdict is one device
+// word per GPU (a file-scope array: its address is looked up once per device, as for
+// the allocation-free entry point's array); checked calls synchronise their stream and
+// are serialised by a lock.
+bool checked_mode()
+{
+    static const bool on = [] {
+        const char* v = getenv("MPM_CHECKED");
+        return v != nullptr && strcmp(v, "1") == 0;
+    }();
+    return on;
+}
+
+static __device__ __align__(16) int32_t check_verdict[4];
+
+constexpr int kMaxCheckDevices = 64;
+std::atomic<int32_t*> g_verdict_ptr[kMaxCheckDevices];
+std::mutex g_check_mutex;  // held across a checked call's validation (one verdict word per GPU)
+
+// Runs `launch_checks(verdict)` on `st` after clearing the verdict, reads it back and
+// returns MPM_OK, MPM_ERR_INVALID_ARG or MPM_ERR_HIP. Called with g_check_mutex held.
+template <class F>
+int run_checks(hipStream_t st, F&& launch_checks)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e);
+    if (dev < 0 || dev >= kMaxCheckDevices) return hip_status(hipErrorInvalidDevice);
+    int32_t* v = g_verdict_ptr[dev].load(std::memory_order_acquire);
+    if (v == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(check_verdict));
+        if (e != hipSuccess) return hip_status(e);
+        if (p == nullptr) return hip_status(hipErrorInvalidSymbol);
+        v = static_cast<int32_t*>(p);
+        g_verdict_ptr[dev].store(v, std::memory_order_release);
+    }
+    e = mpm::launch_zero_words(v, 1, st);
+    if (e == hipSuccess) e = launch_checks(v);
+    int32_t host = 0;
+    if (e == hipSuccess) e = hipMemcpyAsync(&host, v, sizeof host, hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return hip_status(e);
+    return host == 0 ? MPM_OK : MPM_ERR_INVALID_ARG;
+}
+
+// Packed offsets of the rows of x (1 <= n_b <= N), then the rows themselves (finite),
+// their given inverse norms (finite, positive) and grid positions (in range, rows
+// non-decreasing), each where given.
+int checked_rows(const void* x, const int32_t* x_off, const float* x_inv, const int32_t* pos, int grid_w, int32_t B,
+                 int32_t N, int32_t D, int32_t dt, hipStream_t st)
+{
+    std::lock_guard<std::mutex> lock(g_check_mutex);
+    int s = MPM_OK;
+    if (x_off)
+        s = run_checks(st, [&](int32_t* v) { return mpm::launch_check_offsets(x_off, B, N, 1, -1, nullptr, v, st); });
+    if (s != MPM_OK) return s;
+    return run_checks(st, [&](int32_t* v) {
+        hipError_t e = mpm::launch_check_finite(x, x_off, B, N, D, dt, v, st);
+        if (e == hipSuccess && x_inv) e = mpm::launch_check_inv(x_inv, x_off, B, N, v, st);
+        if (e == hipSuccess && pos)
+            e = mpm::launch_check_pos(pos, x_off, B, N, grid_w, (long)grid_w * MPM_MAX_N, v, st);
+        return e;
+    });
+}
+
+// Offsets (where given: x_off for the tokens, y_off for the merged rows, at most n_b of
+// them and within the B*N rows of y), then the slot arrays: neighbours (nb), or the
+// merged rows' sources (src, two per merged row, each below n_b).
+int checked_pairs(const int32_t* x_off, const int32_t* nb, const int32_t* y_off, const int32_t* src, int32_t B,
+                  int32_t N, hipStream_t st)
+{
+    std::lock_guard<std::mutex> lock(g_check_mutex);
+    int s = run_checks(st, [&](int32_t* v) {
+        hipError_t e = hipSuccess;
+        if (x_off) e = mpm::launch_check_offsets(x_off, B, N, 1, -1, nullptr, v, st);
+        if (e == hipSuccess && y_off) e = mpm::launch_check_offsets(y_off, B, N, 1, (long)B * N, x_off, v, st);
+        return e;
+    });
+    if (s != MPM_OK) return s;
+    return run_checks(st, [&](int32_t* v) {
+        if (nb) return mpm::launch_check_nb(nb, x_off, B, N, v, st);
+        return mpm::launch_check_slots(src, 2, y_off, 0, x_off, B, N, mpm::kCheckValues, v, st);
+    });
+}
+
+// Offsets of the merged rows z (where given; P rows per image at most for the padded
+// layout), then maps: map_a in [-1, N) (it indexes map_b's slots, or z's rows when
+// map_b is null) and map_b in [-1, n_z).
+int checked_maps(const int32_t* z_off, int32_t rows_max, const int32_t* map_a, const int32_t* map_b, int32_t B,
+                 int32_t N, hipStream_t st)
+{
+    std::lock_guard<std::mutex> lock(g_check_mutex);
+    int s = MPM_OK;
+    if (z_off)
+        s = run_checks(st, [&](int32_t* v) { return mpm::launch_check_offsets(z_off, B, rows_max, 1, -1, nullptr, v, st); });
+    if (s != MPM_OK || map_a == nullptr) return s;
+    return run_checks(st, [&](int32_t* v) {
+        hipError_t e = mpm::launch_check_slots(map_a, 1, nullptr, -1, map_b ? nullptr : z_off, B, N,
+                                               mpm::kCheckValues, v, st);
+        if (e == hipSuccess && map_b)
+            e = mpm::launch_check_slots(map_b, 1, nullptr, -1, z_off, B, N, mpm::kCheckValues, v, st);
+        return e;
+    });
+}
+
+#define MPM_DATA_CHECK(expr)                                       \
+    do {                                                           \
+        if (checked_mode()) {                                      \
+            const int mpm_checked_status_ = (expr);                \
+            if (mpm_checked_status_ != MPM_OK) return mpm_checked_status_; \
+        }                                                          \
+    } while (0)
+
 int check_shape(int32_t B, int32_t N)
 {
     if (B < 1 || N < 1) return MPM_ERR_INVALID_ARG;
@@ -263,6 +381,7 @@ int mpm_affinity(const void* x, const int32_t* x_off, const float* x_inv, int32_
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_rows(x, x_off, x_inv, nullptr, 1, B, N, D, dt, as_stream(stream)));
     return hip_status(mpm::launch_affinity(x, x_off, B, N, D, dt, schedule, w.pv, w.pi, as_stream(stream),
                                            static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event),
                                            x_inv));
@@ -278,6 +397,7 @@ int mpm_affinity_compact(const void* x, const int32_t* x_off, const float* x_inv
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_rows(x, x_off, x_inv, nullptr, 1, B, N, D, dt, as_stream(stream)));
     return hip_status(affinity_compact(x, x_off, x_inv, B, N, D, dt, schedule, map, y_off, w,
                                        static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event),
                                        as_stream(stream)));
@@ -303,6 +423,7 @@ int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_rows(x, x_off, nullptr, nullptr, 1, B, N, D, dt, as_stream(stream)));
     const hipStream_t st = as_stream(stream);
     hipError_t e = mpm::launch_affinity(x, x_off, B, N, D, dt, schedule, w.pv, w.pi, st, nullptr, nullptr, nullptr);
     if (e == hipSuccess)
@@ -319,6 +440,7 @@ int mpm_pair_compact(const int32_t* nb, const int32_t* x_off, int32_t B, int32_t
     if (!ok_int_ptr(nb) || !ok_opt_int_ptr(x_off) || !ok_int_ptr(map) || !ok_int_ptr(src) || !ok_int_ptr(y_off))
         return MPM_ERR_INVALID_ARG;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_pairs(x_off, nb, nullptr, nullptr, B, N, as_stream(stream)));
     return hip_status(mpm::launch_pair_compact(nb, x_off, B, N, map, src, y_off, nullptr, as_stream(stream)));
 }
 
@@ -331,6 +453,7 @@ int mpm_pair_average(const void* x, const int32_t* x_off, const int32_t* src, co
         !ok_opt_int_ptr(y_inv))
         return MPM_ERR_INVALID_ARG;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_pairs(x_off, nullptr, y_off, src, B, N, as_stream(stream)));
     return hip_status(mpm::launch_pair_average(x, x_off, src, y_off, B, N, D, dt, y, y_inv, as_stream(stream)));
 }
 
@@ -345,6 +468,7 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_rows(x, x_off, x_inv, nullptr, 1, B, N, D, dt, as_stream(stream)));
     const hipStream_t st = as_stream(stream);
     hipError_t e = affinity_compact(x, x_off, x_inv, B, N, D, dt, schedule, map, y_off, w, nullptr, nullptr, st);
     if (e == hipSuccess) e = mpm::launch_pair_average(x, x_off, w.src, y_off, B, N, D, dt, y, y_inv, st);
@@ -360,6 +484,7 @@ int mpm_merge_noalloc(const void* x, const int32_t* x_off, const float* x_inv, i
         return MPM_ERR_INVALID_ARG;
     if (workspace_offsets(B, N).total > kScratchBytes) return MPM_ERR_WORKSPACE;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_rows(x, x_off, x_inv, nullptr, 1, B, N, D, dt, as_stream(stream)));
     const hipStream_t st = as_stream(stream);
     void* ws = nullptr;
     hipError_t e = scratch_for_current_device(st, &ws);
@@ -385,6 +510,7 @@ int mpm_merge_local(const void* x, const int32_t* x_off, const float* x_inv, con
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_rows(x, x_off, x_inv, pos, grid_w, B, N, D, dt, as_stream(stream)));
     const hipStream_t st = as_stream(stream);
     hipError_t e = mpm::launch_affinity_local(x, x_off, x_inv, pos, grid_w, window, B, N, D, dt, w.pv, w.pi, st,
                                               static_cast<hipEvent_t>(start_event),
@@ -402,6 +528,7 @@ int mpm_pad(const void* z, const int32_t* z_off, int32_t B, int32_t P, int32_t r
     if (B > MPM_MAX_B || P > MPM_MAX_N || row_bytes > MPM_MAX_D * 4) return MPM_ERR_UNSUPPORTED;
     if (!ok_rows_ptr(z) || !ok_int_ptr(z_off) || !ok_rows_ptr(out)) return MPM_ERR_INVALID_ARG;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_maps(z_off, P, nullptr, nullptr, B, P, as_stream(stream)));
     return hip_status(mpm::launch_pad(z, z_off, B, P, row_bytes, out, false, as_stream(stream)));
 }
 
@@ -412,6 +539,7 @@ int mpm_unpad(const void* padded, const int32_t* z_off, int32_t B, int32_t P, in
     if (B > MPM_MAX_B || P > MPM_MAX_N || row_bytes > MPM_MAX_D * 4) return MPM_ERR_UNSUPPORTED;
     if (!ok_rows_ptr(padded) || !ok_int_ptr(z_off) || !ok_rows_ptr(z)) return MPM_ERR_INVALID_ARG;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_maps(z_off, P, nullptr, nullptr, B, P, as_stream(stream)));
     return hip_status(mpm::launch_pad(padded, z_off, B, P, row_bytes, z, true, as_stream(stream)));
 }
 
@@ -421,6 +549,7 @@ int mpm_compose(const int32_t* map_a, const int32_t* map_b, int32_t B, int32_t N
     if (s != MPM_OK) return s;
     if (!ok_int_ptr(map_a) || !ok_int_ptr(map_b) || !ok_int_ptr(map_ab)) return MPM_ERR_INVALID_ARG;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_maps(nullptr, N, map_a, map_b, B, N, as_stream(stream)));
     return hip_status(mpm::launch_compose(map_a, map_b, B, N, map_ab, as_stream(stream)));
 }
 
@@ -438,6 +567,7 @@ int mpm_compose_unmerge(const void* z, const int32_t* z_off, const int32_t* map_
         return MPM_ERR_INVALID_ARG;
     if (map_ab != nullptr && (map_ab == map_a || map_ab == map_b)) return MPM_ERR_INVALID_ARG;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_maps(z_off, N, map_a, map_b, B, N, as_stream(stream)));
     return hip_status(mpm::launch_unmerge(z, z_off, map_a, z_spec, E, B, N, D, dt, out, as_stream(stream), map_b,
                                           map_ab));
 }
@@ -452,6 +582,7 @@ int mpm_unmerge(const void* z, const int32_t* z_off, const int32_t* map, const v
     if ((long)E + N > MPM_MAX_N + (long)MPM_MAX_N) return MPM_ERR_UNSUPPORTED;
     if (!ok_rows_ptr(z) || !ok_opt_int_ptr(z_off) || !ok_int_ptr(map) || !ok_rows_ptr(out)) return MPM_ERR_INVALID_ARG;
     MPM_LAUNCH_GATE();
+    MPM_DATA_CHECK(checked_maps(z_off, N, map, nullptr, B, N, as_stream(stream)));
     return hip_status(mpm::launch_unmerge(z, z_off, map, z_spec, E, B, N, D, dt, out, as_stream(stream)));
 }
 

@@ -77,4 +77,27 @@ hipError_t launch_unmerge(const void* z, const int32_t* z_off, const int32_t* ma
                           const void* z_spec, int E, int B, int N, int D, int dt, void* out,
                           hipStream_t stream, const int32_t* map2 = nullptr, int32_t* map_ab = nullptr);
 
+// Checked mode: validation of caller data on the device. Each launcher ORs its bit into
+// *verdict (a device word the caller cleared) when a precondition fails.
+enum CheckBit : int32_t { kCheckOffsets = 1, kCheckValues = 2, kCheckPositions = 4 };
+// Packed offsets: off[0] >= 0, lo_n <= off[b+1] - off[b] <= N, off[B] <= cap (cap >= 0);
+// with `within` (may be null), also at most the count within[b+1] - within[b].
+hipError_t launch_check_offsets(const int32_t* off, int B, int N, int lo_n, long cap, const int32_t* within,
+                                int32_t* verdict, hipStream_t stream);
+// Slot values v[(b*N + i)*per + e] for i below the count of cnt_off (null: N): each in
+// [lo, count of hi_off) (hi_off null: N); `bit` on failure.
+hipError_t launch_check_slots(const int32_t* v, int per, const int32_t* cnt_off, int lo, const int32_t* hi_off, int B,
+                              int N, int32_t bit, int32_t* verdict, hipStream_t stream);
+// Neighbours: nb in [0, n_b) and not the token itself, -1 for a one-token image.
+hipError_t launch_check_nb(const int32_t* nb, const int32_t* x_off, int B, int N, int32_t* verdict, hipStream_t stream);
+// Grid positions: in [0, limit) and non-decreasing in row (pos / grid_w) along each image.
+hipError_t launch_check_pos(const int32_t* pos, const int32_t* x_off, int B, int N, int grid_w, long limit,
+                            int32_t* verdict, hipStream_t stream);
+// Given inverse norms: finite and positive.
+hipError_t launch_check_inv(const float* inv, const int32_t* x_off, int B, int N, int32_t* verdict,
+                            hipStream_t stream);
+// Token values: finite.
+hipError_t launch_check_finite(const void* x, const int32_t* x_off, int B, int N, int D, int dt, int32_t* verdict,
+                               hipStream_t stream);
+
 }  // namespace mpm
