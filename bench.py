@@ -394,7 +394,8 @@ def main() -> int:
 
     schedule = mpm.affinity_schedule_used(cfg.B, cfg.N, cfg.D, dtype, args.schedule)
     if args.window is not None:
-        schedule = f"window {args.window}"
+        rows = mpm.local_block_rows(cfg.B, cfg.N, cfg.D, dtype, cfg.G, args.window)
+        schedule = f"window {args.window}, {rows}-row blocks"
     executed = executed_affinity_flops(cfg, counts, schedule) if args.window is None else None
     kernels = []
     for name, ms, (kind, amount) in zip(names, per_kernel_ms, work):

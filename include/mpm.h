@@ -225,6 +225,19 @@ int mpm_affinity_compact(const void* x, const int32_t* x_off, const float* x_inv
 int mpm_affinity_schedule_used(int32_t B, int32_t N, int32_t D, int32_t dt, int32_t schedule, int32_t* used);
 
 /*
+ * The block size mpm_merge_local's affinity runs for this shape, window and requested
+ * block_rows on the current device, written to *rows (a host pointer): 256 or 128
+ * (square blocks on the symmetric schedule; with block_rows 0, whichever an estimate of
+ * the launch on a full raster grid of grid_w columns, at this window, finds faster), or
+ * N for rows whose byte length is not a multiple of 64 (a kernel that runs each query
+ * block's whole band). For reporting. Returns MPM_OK, MPM_ERR_INVALID_ARG for bad
+ * sizes, grid_w, window or block_rows (as mpm_merge_local) or a NULL pointer, or
+ * MPM_ERR_HIP when the device cannot be queried.
+ */
+int mpm_local_block_rows(int32_t B, int32_t N, int32_t D, int32_t dt, int32_t grid_w, int32_t window,
+                         int32_t block_rows, int32_t* rows);
+
+/*
  * Nearest neighbours: mpm_affinity (norms summed in the kernel), then the
  * reduction of the partials.
  *   nb[b*N + i] = argmax_{j != i, j < n_b} cos(x_i, x_j), lowest j on equal
@@ -293,6 +306,9 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
  *       insertion); positions must be non-decreasing in row along each image;
  *   window >= 0: j is a candidate of i when |row_i - row_j| <= window and
  *       |col_i - col_j| <= window;
+ *   block_rows: 0, 128 or 256: the rows of the square blocks the affinity runs in
+ *       (0: the library's pick, as mpm_local_block_rows reports); results never
+ *       depend on it;
  *   nb[i] = argmax over the candidates of the cosine (lowest j on equal scores), or
  *       -1 when the window holds no other token (i is then a singleton);
  *   y_pos[y_off[b] + k] = the position of cluster k's representative (int32, packed
@@ -302,14 +318,14 @@ int mpm_merge(const void* x, const int32_t* x_off, const float* x_inv, int32_t B
  * Only the candidate tiles a query block's window reaches are computed. The
  * workspace as in mpm_merge (nb and src readable after the call). start_event /
  * stop_event (may be NULL) are bound to the affinity kernel's dispatch, as in
- * mpm_affinity. Errors as
- * mpm_merge, plus MPM_ERR_INVALID_ARG for grid_w < 1, grid_w > MPM_MAX_N or
- * window < 0. Positions outside [0, grid_w * MPM_MAX_N) are undefined behaviour.
+ * mpm_affinity. Errors as mpm_merge, plus MPM_ERR_INVALID_ARG for grid_w < 1,
+ * grid_w > MPM_MAX_N, window < 0 or another block_rows. Positions outside
+ * [0, grid_w * MPM_MAX_N) are undefined behaviour.
  */
 int mpm_merge_local(const void* x, const int32_t* x_off, const float* x_inv, const int32_t* pos, int32_t B,
-                    int32_t N, int32_t D, int32_t dt, int32_t grid_w, int32_t window, void* y, int32_t* y_off,
-                    float* y_inv, int32_t* y_pos, int32_t* map, void* ws, size_t ws_bytes, void* start_event,
-                    void* stop_event, void* stream);
+                    int32_t N, int32_t D, int32_t dt, int32_t grid_w, int32_t window, int32_t block_rows, void* y,
+                    int32_t* y_off, float* y_inv, int32_t* y_pos, int32_t* map, void* ws, size_t ws_bytes,
+                    void* start_event, void* stop_event, void* stream);
 
 /*
  * Padded batch layout (the paper pads each batch to its longest image, Sec. 4.2): the

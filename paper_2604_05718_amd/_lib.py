@@ -43,12 +43,14 @@ SIGNATURES = {
     "mpm_affinity_compact": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp, _vp,
                                             _vp]),
     "mpm_affinity_schedule_used": (ctypes.c_int, [_i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_int32)]),
+    "mpm_local_block_rows": (ctypes.c_int, [_i32, _i32, _i32, _i32, _i32, _i32, _i32,
+                                            ctypes.POINTER(ctypes.c_int32)]),
     "mpm_argmax": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _sz, _vp]),
     "mpm_pair_compact": (ctypes.c_int, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp]),
     "mpm_pair_average": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp, _vp]),
     "mpm_merge": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
-    "mpm_merge_local": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp,
-                                       _vp, _vp, _sz, _vp, _vp, _vp]),
+    "mpm_merge_local": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp,
+                                       _vp, _vp, _vp, _sz, _vp, _vp, _vp]),
     "mpm_merge_noalloc": (ctypes.c_int, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
     "mpm_pad": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _vp, _vp]),
     "mpm_unpad": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _vp, _vp]),

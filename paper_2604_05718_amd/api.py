@@ -147,6 +147,18 @@ def affinity_schedule_used(B: int, N: int, D: int, dtype: torch.dtype, schedule:
     return {v: k for k, v in SCHEDULES.items()}[out.value]
 
 
+def local_block_rows(B: int, N: int, D: int, dtype: torch.dtype, grid_w: int, window: int,
+                     block_rows: int = 0) -> int:
+    """Rows of the square blocks merge_local's affinity runs for this shape, window and
+    requested block_rows (0: the library's pick) on the current device (256 or 128; N
+    for rows the persistent kernel does not take)."""
+    out = ctypes.c_int32()
+    _lib.check("mpm_local_block_rows", _lib.load().mpm_local_block_rows(B, N, D, _DTYPES[dtype], int(grid_w),
+                                                                        int(window), int(block_rows),
+                                                                        ctypes.byref(out)))
+    return out.value
+
+
 def ws_view(ws: torch.Tensor, B: int, N: int, region: str) -> torch.Tensor:
     """A workspace region as an int32 view: "nb" [B, N] or "src" [B, N, 2]."""
     off = _lib.workspace_offsets(B, N)[region]
@@ -221,11 +233,12 @@ def insertion(x, x_off=None, N=None, x_inv=None, want_inv=False, ws=None, schedu
 
 
 def merge_local(x, grid_w: int, window: int, x_off=None, N=None, pos=None, ws=None, x_inv=None,
-                want_inv=False) -> Merged:
+                want_inv=False, block_rows: int = 0) -> Merged:
     """One locality-constrained insertion (Sec. 5): candidates within ``window`` rows and
     columns on a grid of ``grid_w`` columns; ``pos`` the tokens' raster positions
     (packed like x; None: each token's index in its image). The merged rows'
-    positions are returned in ``y_pos``; ``x_inv`` / ``want_inv`` as in merge()."""
+    positions are returned in ``y_pos``; ``x_inv`` / ``want_inv`` as in merge();
+    ``block_rows`` 128 or 256 forces the affinity's block size (0: the library's pick)."""
     x2, B, N, D = _rows(x, N, x_off)
     dev = x.device
     ws = _workspace(B, N, dev, ws)
@@ -235,9 +248,9 @@ def merge_local(x, grid_w: int, window: int, x_off=None, N=None, pos=None, ws=No
     m = torch.empty((B, N), dtype=torch.int32, device=dev)
     y_inv = torch.empty((B * N,), dtype=torch.float32, device=dev) if want_inv else None
     _lib.check("mpm_merge_local", _lib.load().mpm_merge_local(_p(x2), _p(x_off), _p(x_inv), _p(pos), B, N, D, _dt(x),
-                                                              int(grid_w), int(window), _p(y), _p(y_off), _p(y_inv),
-                                                              _p(y_pos), _p(m), _p(ws), ws.numel(), None, None,
-                                                              _stream()))
+                                                              int(grid_w), int(window), int(block_rows), _p(y),
+                                                              _p(y_off), _p(y_inv), _p(y_pos), _p(m), _p(ws),
+                                                              ws.numel(), None, None, _stream()))
     return Merged(y, y_off, m, ws, B, N, y_inv, y_pos)
 
 
@@ -316,13 +329,13 @@ class ScheduleResult:
 
 
 def run_schedule(x, insertions: int = 2, workspaces=None, schedule: str = "auto", grid_w: int | None = None,
-                 window: int | None = None) -> ScheduleResult:
+                 window: int | None = None, block_rows: int = 0) -> ScheduleResult:
     """Insertions with identity blocks in between (Sec. 3.3), composed maps
     (Eq. 3) and one gather back to the full grid (Eq. 4). Each insertion after the
     first takes the inverse norms of its input rows from the pair average that
     wrote them (rows a whole number of 64 bytes), as Schedule does. With
-    ``window``, every insertion is locality-constrained (merge_local) on a grid of
-    ``grid_w`` columns, the first on the raster positions."""
+    ``window``, every insertion is locality-constrained (merge_local, with
+    ``block_rows``) on a grid of ``grid_w`` columns, the first on the raster positions."""
     B, N, D = x.shape
     norms = takes_norms(D, x.dtype)
     stages = []
@@ -332,7 +345,7 @@ def run_schedule(x, insertions: int = 2, workspaces=None, schedule: str = "auto"
         ws = None if workspaces is None else workspaces[s]
         if window is not None:
             m = merge_local(cur, grid_w, window, x_off=cur_off, N=N, pos=cur_pos, ws=ws, x_inv=cur_inv,
-                            want_inv=norms and s + 1 < insertions)
+                            want_inv=norms and s + 1 < insertions, block_rows=block_rows)
         else:
             m = merge(cur, cur_off, N=N, x_inv=cur_inv, want_inv=norms and s + 1 < insertions, ws=ws,
                       schedule=schedule)
@@ -422,7 +435,7 @@ class Schedule:
             if self.window is not None:
                 ev0, ev1 = (None, None) if affinity_events is None else (c_event(e) for e in affinity_events[s])
                 _lib.check("mpm_merge_local", lib.mpm_merge_local(
-                    _p(cur), _p(cur_off), _p(cur_inv), _p(cur_pos), B, N, D, dt, self.grid_w, self.window,
+                    _p(cur), _p(cur_off), _p(cur_inv), _p(cur_pos), B, N, D, dt, self.grid_w, self.window, 0,
                     _p(self.y[s]), _p(self.y_off[s]), _p(self.y_inv[s]), _p(self.y_pos[s]), _p(self.map[s]), _p(ws),
                     ws.numel(), ev0, ev1, st))
                 cur, cur_off, cur_inv, cur_pos = self.y[s], self.y_off[s], self.y_inv[s], self.y_pos[s]

@@ -25,6 +25,9 @@
 // tile and no separate normalisation pass exists.
 #include <hip/hip_ext.h>
 
+#include <algorithm>
+#include <vector>
+
 #include "mpm_device.h"
 #include "mpm_launch.h"
 
@@ -1356,9 +1359,58 @@ bool symmetric_schedule(int B, int N, int xcds, int slots, int schedule)
     return 5 * sym < 4 * full;
 }
 
+// The locality-constrained schedule's two block sizes: 256 x 256 blocks on 8 waves, one
+// workgroup per CU (the dense symmetric shape), or 128 x 128 blocks on 4 waves of 64 x 64,
+// two workgroups per CU. Smaller blocks cut a query block's window band more finely and
+// give twice the items; each small block costs about 0.357 of a large one (a quarter of
+// its matrix work at about 70% of its efficiency: half the flops per byte loaded).
+constexpr int kLWC = 2, kLWQ = 2, kLMT = 2, kLNT = 2, kLWGS = 2;
+constexpr int kLCT = kLWC * kLMT * 32;
+static_assert(kLWQ * kLNT * 32 == kLCT && kPCT % kLCT == 0 && kLCT % kTCT == 0, "square small window blocks");
+constexpr double kLSmallBlockCost = 0.357;
+
+// Estimated duration (in large-block times) of a locality-constrained launch with ts x ts
+// blocks, on a full raster grid (positions = token indices): per XCD group, the blocks of
+// its images are dealt to the slots in order, each costing the tiles of its band from its
+// own on. With two workgroups per CU, the busiest slot is taken to share its CU with a
+// typical (median) one.
+double local_cost(int B, int N, int grid_w, int radius, int ts, int xcds, int slots, int wgs_per_cu, double block_cost)
+{
+    const int nblk = (N + ts - 1) / ts;
+    std::vector<int> tiles(nblk);
+    long total = 0;
+    for (int t = 0; t < nblk; ++t) {
+        const long r_last = (long)(std::min((t + 1) * ts, N) - 1) / grid_w;
+        const long thi = std::min<long>(nblk - 1, ((r_last + radius + 1) * (long)grid_w - 1) / ts);
+        tiles[t] = (int)(thi - t + 1);
+        total += tiles[t];
+    }
+    const long imgs = (B + xcds - 1) / xcds;  // images of the largest group
+    const long items = imgs * nblk;
+    if (items > 64L * slots) return (double)imgs * total / slots * wgs_per_cu * block_cost;  // many rounds: balanced
+    std::vector<long> load(slots, 0);
+    for (long k = 0; k < items; ++k) load[k % slots] += tiles[k % nblk];
+    std::sort(load.begin(), load.end());
+    const long busiest = load[slots - 1];
+    const long typical = load[slots / 2];
+    return (double)(wgs_per_cu == 1 ? busiest : busiest + typical) * block_cost;
+}
+
 }  // namespace
 
-int local_partial_tile_width(int D, int dt, int N) { return use_persistent(D, dt) ? kPCT : N; }
+bool valid_local_block_rows(int requested) { return requested == 0 || requested == kLCT || requested == kPCT; }
+
+int local_block_rows(int B, int N, int D, int dt, int grid_w, int radius, int requested)
+{
+    if (!use_persistent(D, dt)) return N;
+    if (requested != 0) return requested;
+    const int cus = device_cus();
+    if (cus <= 0) return kPCT;
+    const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
+    const double large = local_cost(B, N, grid_w, radius, kPCT, xcds, cus * kPWGS / xcds, kPWGS, 1.0);
+    const double small = local_cost(B, N, grid_w, radius, kLCT, xcds, cus * kLWGS / xcds, kLWGS, kLSmallBlockCost);
+    return small < large ? kLCT : kPCT;
+}
 
 int partial_tile_width(int B, int D, int dt, int N, int schedule)
 {
@@ -1425,7 +1477,7 @@ hipError_t launch_affinity(const void* x, const int32_t* x_off, int B, int N, in
 }
 
 hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const float* xinv, const int32_t* pos,
-                                 int grid_w, int radius,
+                                 int grid_w, int radius, int block_rows,
                                  int B, int N, int D, int dt, float* pv, int32_t* pi, hipStream_t stream,
                                  hipEvent_t start, hipEvent_t stop)
 {
@@ -1433,16 +1485,28 @@ hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const floa
     const Window win{pos, grid_w, radius};
     if (use_persistent(D, dt)) {
         // The persistent kernel on the symmetric schedule, one item per query block and the
-        // tiles of its band from its own on (given norms: bf16 only).
+        // tiles of its band from its own on (given norms: bf16 only), with the block size
+        // local_block_rows picks (block_rows: the caller's, 0 to estimate it here).
         const int cus = device_cus();
         if (cus <= 0) return hipErrorInvalidDevice;
         const int xcds = (cus % kXcds == 0 && B >= kXcds) ? kXcds : 1;
-        if (dt == kBf16)
-            launch_persistent<Bf16, kSWC, kSWQ, kSMT, kSNT, true, true>(x, x_off, xinv, B, N, D, T, xcds,
-                                                                        cus * kPWGS, pv, pi, stream, start, stop, win);
-        else
-            launch_persistent<F32, kSWC, kSWQ, kSMT, kSNT, true, true>(x, x_off, nullptr, B, N, D, T, xcds,
-                                                                       cus * kPWGS, pv, pi, stream, start, stop, win);
+        const bool small = local_block_rows(B, N, D, dt, grid_w, radius, block_rows) == kLCT;
+        if (small) {
+            if (dt == kBf16)
+                launch_persistent<Bf16, kLWC, kLWQ, kLMT, kLNT, true, true>(x, x_off, xinv, B, N, D, T, xcds,
+                                                                            cus * kLWGS, pv, pi, stream, start, stop,
+                                                                            win);
+            else
+                launch_persistent<F32, kLWC, kLWQ, kLMT, kLNT, true, true>(x, x_off, nullptr, B, N, D, T, xcds,
+                                                                           cus * kLWGS, pv, pi, stream, start, stop,
+                                                                           win);
+        } else if (dt == kBf16) {
+            launch_persistent<Bf16, kSWC, kSWQ, kSMT, kSNT, true, true>(x, x_off, xinv, B, N, D, T, xcds, cus * kPWGS,
+                                                                        pv, pi, stream, start, stop, win);
+        } else {
+            launch_persistent<F32, kSWC, kSWQ, kSMT, kSNT, true, true>(x, x_off, nullptr, B, N, D, T, xcds, cus * kPWGS,
+                                                                       pv, pi, stream, start, stop, win);
+        }
         return hipGetLastError();
     }
     if (dt == kBf16)

@@ -414,6 +414,19 @@ int mpm_affinity_schedule_used(int32_t B, int32_t N, int32_t D, int32_t dt, int3
     return st;
 }
 
+int mpm_local_block_rows(int32_t B, int32_t N, int32_t D, int32_t dt, int32_t grid_w, int32_t window,
+                         int32_t block_rows, int32_t* rows)
+{
+    const int s = check_rows(B, N, D, dt);
+    if (s != MPM_OK) return s;
+    if (!rows || grid_w < 1 || grid_w > MPM_MAX_N || window < 0 || !mpm::valid_local_block_rows(block_rows))
+        return MPM_ERR_INVALID_ARG;
+    int dev = 0;
+    const int st = hip_status(hipGetDevice(&dev));
+    if (st == MPM_OK) *rows = mpm::local_block_rows(B, N, D, dt, grid_w, window, block_rows);
+    return st;
+}
+
 int mpm_argmax(const void* x, const int32_t* x_off, int32_t B, int32_t N, int32_t D, int32_t dt, int32_t schedule,
                int32_t* nb, float* best, void* ws, size_t ws_bytes, void* stream)
 {
@@ -497,26 +510,28 @@ int mpm_merge_noalloc(const void* x, const int32_t* x_off, const float* x_inv, i
 }
 
 int mpm_merge_local(const void* x, const int32_t* x_off, const float* x_inv, const int32_t* pos, int32_t B,
-                    int32_t N, int32_t D, int32_t dt, int32_t grid_w, int32_t window, void* y, int32_t* y_off,
-                    float* y_inv, int32_t* y_pos, int32_t* map, void* ws, size_t ws_bytes, void* start_event,
-                    void* stop_event, void* stream)
+                    int32_t N, int32_t D, int32_t dt, int32_t grid_w, int32_t window, int32_t block_rows, void* y,
+                    int32_t* y_off, float* y_inv, int32_t* y_pos, int32_t* map, void* ws, size_t ws_bytes,
+                    void* start_event, void* stop_event, void* stream)
 {
     int s = check_affinity(x, x_off, x_inv, B, N, D, dt, MPM_SCHEDULE_AUTO);
     if (s != MPM_OK) return s;
     if (!ok_opt_int_ptr(pos) || !ok_rows_ptr(y) || !ok_int_ptr(y_off) || !ok_opt_int_ptr(y_inv) ||
         !ok_int_ptr(y_pos) || !ok_int_ptr(map))
         return MPM_ERR_INVALID_ARG;
-    if (grid_w < 1 || grid_w > MPM_MAX_N || window < 0) return MPM_ERR_INVALID_ARG;
+    if (grid_w < 1 || grid_w > MPM_MAX_N || window < 0 || !mpm::valid_local_block_rows(block_rows))
+        return MPM_ERR_INVALID_ARG;
     Workspace w;
     if ((s = carve(ws, ws_bytes, B, N, &w)) != MPM_OK) return s;
     MPM_LAUNCH_GATE();
     MPM_DATA_CHECK(checked_rows(x, x_off, x_inv, pos, grid_w, B, N, D, dt, as_stream(stream)));
     const hipStream_t st = as_stream(stream);
-    hipError_t e = mpm::launch_affinity_local(x, x_off, x_inv, pos, grid_w, window, B, N, D, dt, w.pv, w.pi, st,
+    const int rows = mpm::local_block_rows(B, N, D, dt, grid_w, window, block_rows);
+    hipError_t e = mpm::launch_affinity_local(x, x_off, x_inv, pos, grid_w, window, rows, B, N, D, dt, w.pv, w.pi, st,
                                               static_cast<hipEvent_t>(start_event),
                                               static_cast<hipEvent_t>(stop_event));
     if (e == hipSuccess)
-        e = compact_partials_ct(w, x_off, B, N, D, dt, mpm::local_partial_tile_width(D, dt, N), map, y_off, st);
+        e = compact_partials_ct(w, x_off, B, N, D, dt, rows, map, y_off, st);
     if (e == hipSuccess)
         e = mpm::launch_pair_average(x, x_off, w.src, y_off, B, N, D, dt, y, y_inv, st, pos, y_pos);
     return hip_status(e);

@@ -27,9 +27,12 @@ bool affinity_takes_norms(int D, int dt);
 int partial_tiles(int N);
 // Candidate rows covered by one partial of the kernel launch_affinity picks for this call.
 int partial_tile_width(int B, int D, int dt, int N, int schedule);
-// ... and of launch_affinity_local's kernel (one partial slot per 256-row block on the
-// persistent kernel's symmetric schedule, else one slot covering the image).
-int local_partial_tile_width(int D, int dt, int N);
+// ... and of launch_affinity_local's kernel: the rows of its square blocks on the
+// persistent kernel's symmetric schedule (`requested`, 128 or 256; 0: whichever an
+// estimate of the launch on a full raster grid of grid_w columns finds faster on the
+// current device), else N (one slot covering the image).
+int local_block_rows(int B, int N, int D, int dt, int grid_w, int radius, int requested);
+bool valid_local_block_rows(int requested);
 // The schedule (kScheduleFull, kScheduleSymmetric or kScheduleFull64) launch_affinity runs
 // for this shape and requested schedule on the current device.
 hipError_t affinity_schedule(int B, int N, int D, int dt, int schedule, int* used);
@@ -56,10 +59,10 @@ hipError_t launch_pair_average(const void* x, const int32_t* x_off, const int32_
 // restricted to the cells within `radius` rows and columns of its own on a grid of
 // grid_w columns (pos: raster positions packed like x, or null for each token's index;
 // xinv: given inverse norms, or null to sum them); partials of
-// local_partial_tile_width(D, dt, N) candidate rows each, every slot of an image's tiles
-// written (-inf, -1 where the window reaches no candidate of a tile).
+// local_block_rows(B, N, D, dt, grid_w, radius, block_rows) candidate rows each, every
+// slot of an image's tiles written (-inf, -1 where the window reaches no candidate of a tile).
 hipError_t launch_affinity_local(const void* x, const int32_t* x_off, const float* xinv, const int32_t* pos,
-                                 int grid_w, int radius,
+                                 int grid_w, int radius, int block_rows,
                                  int B, int N, int D, int dt, float* pv, int32_t* pi, hipStream_t stream,
                                  hipEvent_t start, hipEvent_t stop);
 

@@ -149,8 +149,8 @@ def test_pad_unpad_and_local_reject(lib):
     def local(**kw):
         a = dict(ok, **kw)
         return lib.mpm_merge_local(A, None, a.get("x_inv"), a["pos"], 2, 64, a.get("D", 64), a.get("dt", 1),
-                                   a["grid_w"], a["window"], A2, A2, a.get("y_inv"), a["y_pos"], A2, A2,
-                                   a.get("ws", ws), None, None, None)
+                                   a["grid_w"], a["window"], a.get("block_rows", 0), A2, A2, a.get("y_inv"),
+                                   a["y_pos"], A2, A2, a.get("ws", ws), None, None, None)
     assert local(grid_w=0) == 1
     assert local(grid_w=16385) == 1
     assert local(window=-1) == 1
@@ -162,6 +162,16 @@ def test_pad_unpad_and_local_reject(lib):
     assert local(y_inv=odd) == 1
     assert local(x_inv=A, D=40) == 2                          # given norms: 80-byte rows
     assert local(x_inv=A, dt=0) == 2                          # given norms: float32 rows
+    for rows in (64, 192, 512, -1):
+        assert local(block_rows=rows) == 1                    # block sizes: 0, 128 or 256
+    out = ctypes.c_int32(-7)
+    query = lib.mpm_local_block_rows
+    assert query(2, 64, 64, 1, 8, 1, 0, None) == 1            # NULL output
+    assert query(2, 64, 64, 1, 0, 1, 0, ctypes.byref(out)) == 1
+    assert query(2, 64, 64, 1, 8, -1, 0, ctypes.byref(out)) == 1
+    assert query(2, 64, 64, 1, 8, 1, 96, ctypes.byref(out)) == 1
+    assert query(0, 64, 64, 1, 8, 1, 0, ctypes.byref(out)) == 1
+    assert out.value == -7
     assert lib.mpm_last_hip_error() == 0
 
 

@@ -82,7 +82,7 @@ def local(pos):
     yo = torch.full((B + 1,), -7, dtype=torch.int32, device=dev)
     yp = torch.zeros((B * N,), dtype=torch.int32, device=dev)
     m = torch.full((B, N), -7, dtype=torch.int32, device=dev)
-    rc = lib.mpm_merge_local(P(x), P(x_off), None, P(pos), B, N, D, 1, 20, 2, P(y), P(yo), None, P(yp), P(m), P(ws),
+    rc = lib.mpm_merge_local(P(x), P(x_off), None, P(pos), B, N, D, 1, 20, 2, 0, P(y), P(yo), None, P(yp), P(m), P(ws),
                              wsb, None, None, st)
     torch.cuda.synchronize()
     return rc, untouched(yo, m)

@@ -95,13 +95,15 @@ CASES = [  # (grid rows, grid cols, D, window, images)
     (24, 24, 64, 3, 9)]
 
 
+@pytest.mark.parametrize("block_rows", [128, 256])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("gh,gw,D,window,B", CASES)
-def test_local_schedule_random_grids(dtype, gh, gw, D, window, B):
+def test_local_schedule_random_grids(dtype, gh, gw, D, window, B, block_rows):
     """Two windowed insertions on clustered tokens (the second on the ragged packed
     survivors and their carried positions), composition and gather, every image
-    checked; window 0 leaves every token alone, a window covering the grid is the
-    dense method."""
+    checked, with either block size of the persistent kernel (rows that are not a
+    whole number of 64 bytes take the register-staged kernel either way); window 0
+    leaves every token alone, a window covering the grid is the dense method."""
     rng = np.random.default_rng(gh * 1000 + gw * 10 + window)
     N = gh * gw
     imgs = []
@@ -110,8 +112,8 @@ def test_local_schedule_random_grids(dtype, gh, gw, D, window, B):
         lab = rng.integers(0, 12, N)
         imgs.append(store(cent[lab] + 0.3 * rng.standard_normal((N, D)), dtype))
     x = torch.stack(imgs)
-    print(f"local schedule {dtype} grid {gh}x{gw} D={D} window={window} B={B}", flush=True)
-    res = mpm.run_schedule(x.to(DEV), insertions=2, grid_w=gw, window=window)
+    print(f"local schedule {dtype} grid {gh}x{gw} D={D} window={window} B={B} blocks {block_rows}", flush=True)
+    res = mpm.run_schedule(x.to(DEV), insertions=2, grid_w=gw, window=window, block_rows=block_rows)
     torch.cuda.synchronize()
     for b in range(B):
         check_local_schedule_image(x[b], dtype, res, b, gw, window)
@@ -127,7 +129,8 @@ def test_local_schedule_full_size(name, window, images):
     bench.py --window times), sampled images checked completely."""
     cfg = synth.config(name)
     x = synth.make_batch(cfg, seed=0)
-    print(f"local schedule {name} window={window}: B={cfg.B} N={cfg.N} D={cfg.D}", flush=True)
+    rows = mpm.local_block_rows(cfg.B, cfg.N, cfg.D, x.dtype, cfg.G, window)
+    print(f"local schedule {name} window={window}: B={cfg.B} N={cfg.N} D={cfg.D}, {rows}-row blocks", flush=True)
     res = mpm.run_schedule(x.to(DEV), insertions=cfg.insertions, grid_w=cfg.G, window=window)
     torch.cuda.synchronize()
     flips = sum(check_local_schedule_image(x[b], cfg.dtype, res, b, cfg.G, window) for b in images)
@@ -135,9 +138,10 @@ def test_local_schedule_full_size(name, window, images):
     print(f"  survivors (mean): {[round(sum(c) / len(c), 1) for c in counts]}, accepted flips {flips}", flush=True)
 
 
+@pytest.mark.parametrize("block_rows", [128, 256])
 @pytest.mark.parametrize("dtype,given_norms", [("f32", False), ("bf16", False), ("bf16", True)])
 @pytest.mark.parametrize("given_pos", [False, True])
-def test_local_packed_edge_images(dtype, given_norms, given_pos):
+def test_local_packed_edge_images(dtype, given_norms, given_pos, block_rows):
     """One windowed insertion on packed ragged images: empty, one-token and two-token
     images, images ending inside a grid row and inside a 256-token block, nine images
     (the persistent kernel's per-XCD image groups), positions either each token's index
@@ -158,8 +162,10 @@ def test_local_packed_edge_images(dtype, given_norms, given_pos):
     if given_norms:
         inv = np.concatenate([1.0 / np.maximum(np.sqrt((r ** 2).sum(axis=1)), 1e-12) for r in x64])
         x_inv = torch.from_numpy(inv.astype(np.float32)).to(DEV)
-    print(f"local packed {dtype} given_norms={given_norms} given_pos={given_pos}: images {ns}", flush=True)
-    res = mpm.merge_local(x, grid_w, window, x_off=xo, N=max(ns), pos=pos, x_inv=x_inv, want_inv=True)
+    print(f"local packed {dtype} given_norms={given_norms} given_pos={given_pos} blocks {block_rows}: images {ns}",
+          flush=True)
+    res = mpm.merge_local(x, grid_w, window, x_off=xo, N=max(ns), pos=pos, x_inv=x_inv, want_inv=True,
+                          block_rows=block_rows)
     torch.cuda.synchronize()
     y_off = res.y_off.cpu().numpy()
     for b, n in enumerate(ns):
@@ -188,3 +194,20 @@ def test_local_packed_edge_images(dtype, given_norms, given_pos):
         yi = res.y_inv[y_off[b]:y_off[b + 1]].cpu().numpy().astype(np.float64)
         want = 1.0 / np.maximum(np.sqrt((y ** 2).sum(axis=1)), 1e-12)
         assert np.max(np.abs(yi / want - 1.0)) <= 1e-5, f"image {b}: merged inverse norms"
+
+
+def test_local_block_choice():
+    """The block size the library picks for the windowed benchmark workloads on this
+    device (an estimate on a full raster grid; 256 CUs): 256-row blocks where a 128-row
+    block's band would reach two blocks past its own (ViT-L/16 at 1024 px, window 4),
+    128-row blocks elsewhere; a forced size is reported as forced."""
+    picks = {}
+    for name, window in [("vit_l_1024", 4), ("vit_l_1024", 2), ("vit_b_512", 3), ("stress_768", 4)]:
+        cfg = synth.config(name)
+        picks[(name, window)] = mpm.local_block_rows(cfg.B, cfg.N, cfg.D, TORCH_DT[cfg.dtype], cfg.G, window)
+    print(f"block rows: {picks}", flush=True)
+    if torch.cuda.get_device_properties(DEV).multi_processor_count != 256:
+        pytest.skip("the picks below are for a 256-CU device")
+    assert picks == {("vit_l_1024", 4): 256, ("vit_l_1024", 2): 128, ("vit_b_512", 3): 128, ("stress_768", 4): 128}
+    assert mpm.local_block_rows(16, 4096, 1024, torch.bfloat16, 64, 4, block_rows=128) == 128
+    assert mpm.local_block_rows(16, 4096, 40, torch.bfloat16, 64, 4) == 4096   # 80-byte rows: the staged kernel
