@@ -62,6 +62,25 @@ int main(void)
     EXPECT(mpm_unmerge(A, NULL, A, NULL, -1, 2, 8, 64, MPM_BF16, A, NULL), MPM_ERR_INVALID_ARG);
     EXPECT(mpm_compose_unmerge(A, NULL, A, A2, A, NULL, 0, 2, 8, 64, MPM_BF16, A, NULL), MPM_ERR_INVALID_ARG);
     EXPECT(mpm_workspace_init(MIS, big, NULL), MPM_ERR_INVALID_ARG);
+    EXPECT(mpm_merge_local(A, NULL, NULL, NULL, 2, 64, 64, MPM_BF16, 0, 1, 0, A2, A2, NULL, A2, A2, A, big, NULL, NULL,
+                           NULL), MPM_ERR_INVALID_ARG);                                 /* grid_w < 1 */
+    EXPECT(mpm_merge_local(A, NULL, NULL, NULL, 2, 64, 64, MPM_BF16, 8, -1, 0, A2, A2, NULL, A2, A2, A, big, NULL, NULL,
+                           NULL), MPM_ERR_INVALID_ARG);                                 /* window < 0 */
+    EXPECT(mpm_merge_local(A, NULL, NULL, NULL, 2, 64, 64, MPM_BF16, 8, 1, 64, A2, A2, NULL, A2, A2, A, big, NULL, NULL,
+                           NULL), MPM_ERR_INVALID_ARG);                                 /* block_rows */
+    EXPECT(mpm_merge_local(A, NULL, A, NULL, 2, 64, 40, MPM_BF16, 8, 1, 0, A2, A2, NULL, A2, A2, A, big, NULL, NULL,
+                           NULL), MPM_ERR_UNSUPPORTED);                                 /* norms, 80-byte rows */
+    EXPECT(mpm_merge_local(A, NULL, NULL, NULL, 2, 64, 64, MPM_BF16, 8, 1, 0, A2, A2, NULL, A2, A2, A, 16, NULL, NULL,
+                           NULL), MPM_ERR_WORKSPACE);
+    {
+        int32_t rows = -7;
+        EXPECT(mpm_local_block_rows(2, 64, 64, MPM_BF16, 8, 1, 0, NULL), MPM_ERR_INVALID_ARG);
+        EXPECT(mpm_local_block_rows(2, 64, 64, MPM_BF16, 8, 1, 100, &rows), MPM_ERR_INVALID_ARG);
+        EXPECT(mpm_local_block_rows(2, 64, 64, MPM_BF16, MPM_MAX_N + 1, 1, 0, &rows), MPM_ERR_INVALID_ARG);
+        if (rows != -7) return 1;
+    }
+    EXPECT(mpm_pad(A, A2, 2, 8, 40, A, NULL), MPM_ERR_INVALID_ARG);
+    EXPECT(mpm_unpad(A, NULL, 2, 8, 64, A, NULL), MPM_ERR_INVALID_ARG);
     EXPECT(mpm_last_hip_error(), 0);
     if (mpm_status_string(42) == NULL || strcmp(mpm_status_string(MPM_ERR_HIP), "MPM_ERR_HIP") != 0) return 1;
 
@@ -81,6 +100,10 @@ int main(void)
         EXPECT(mpm_compose(A, A2, 2, 16, A, NULL), MPM_ERR_HIP);
         EXPECT(mpm_unmerge(A, NULL, A2, NULL, 0, 2, 16, 64, MPM_BF16, A, NULL), MPM_ERR_HIP);
         EXPECT(mpm_compose_unmerge(A, NULL, A2, A2, NULL, NULL, 0, 2, 16, 64, MPM_BF16, A, NULL), MPM_ERR_HIP);
+        EXPECT(mpm_merge_local(A, NULL, NULL, NULL, 2, 64, 64, MPM_BF16, 8, 1, 0, A2, A2, NULL, A2, A2, A, big, NULL,
+                               NULL, NULL), MPM_ERR_HIP);
+        EXPECT(mpm_pad(A, A2, 2, 8, 64, A, NULL), MPM_ERR_HIP);
+        EXPECT(mpm_unpad(A, A2, 2, 8, 64, A, NULL), MPM_ERR_HIP);
         EXPECT(mpm_last_hip_error(), hip_launch_failure);
     }
     printf("abi driver: ok%s\n", inject ? " (with injected launch failures)" : "");
