@@ -33,9 +33,9 @@ METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak
 # rocprofv3 FETCH_SIZE / WRITE_SIZE runs on each workload, calibrated with a copy
 # kernel (profiles/<workload>_rocprof.md). Valid only for the kernel source it was
 # measured on, with the default schedule.
-TRAFFIC = {"source_sha256": "2fb495c0be3689dd42a16ec72984b3d2bf1fb568a0c14d070854d2f6db479dec",
-           "bytes_per_launch": {"vit_ti_512": 6552793, "vit_s_512": 25826021, "vit_b_512": 151186255,
-                                "vit_l_1024": 510338159, "stress_768": 182548622}}
+TRAFFIC = {"source_sha256": "1dae8e815f91dc3ce104e116133adef4251abc9e32c244ab1520b8269f69403b",
+           "bytes_per_launch": {"vit_ti_512": 6556908, "vit_s_512": 25826093, "vit_b_512": 151371046,
+                                "vit_l_1024": 510609428, "stress_768": 181822003}}
 
 
 def log(*a):
