@@ -25,7 +25,7 @@ namespace {
 
 constexpr int kCompactThreads = 1024;
 constexpr int kCompactWaves = kCompactThreads / kWave;
-constexpr int kPartialBatch = 4;  // partial tiles whose loads are issued together
+constexpr int kPartialBatch = 8;  // partial tiles whose loads are issued together (16 spilled)
 constexpr int kDoneSlot = 65535;  // sync-region slot of the images-done counter
 
 __device__ __forceinline__ bool is_mutual(const int32_t* nbl, int i, int j, int n)
