@@ -64,8 +64,9 @@
  *   or [-1, n_z) where they index merged rows). Offsets are validated first; the
  *   rows they address must exist. On a violation the call returns
  *   MPM_ERR_INVALID_ARG and launches nothing of its operation. A checked call
- *   synchronises its stream (it reads the verdict back), and checked calls are
- *   serialised by a lock. Without the variable nothing of this runs.
+ *   synchronises its stream (it reads the verdict back; so not under graph
+ *   capture), and checked calls are serialised by a lock. Without the variable
+ *   nothing of this runs.
  */
 #ifndef MPM_H
 #define MPM_H
