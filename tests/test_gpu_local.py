@@ -122,16 +122,24 @@ def test_local_schedule_random_grids(dtype, gh, gw, D, window, B, block_rows):
 
 
 @pytest.mark.timeout(900)
+@pytest.mark.parametrize("forced", [False, True])
 @pytest.mark.parametrize("name,window,images", [("vit_b_512", 3, [0, 21, 63]), ("vit_l_1024", 4, [0, 9, 15]),
                                                  ("stress_768", 4, [0, 5, 31])])
-def test_local_schedule_full_size(name, window, images):
-    """The windowed schedule on a full benchmark batch (the launch configuration
-    bench.py --window times), sampled images checked completely."""
+def test_local_schedule_full_size(name, window, images, forced):
+    """The windowed schedule on a full benchmark batch: with the block size the library
+    picks (the launch configuration bench.py --window times), every image checked
+    completely; with the other block size forced, sampled images."""
     cfg = synth.config(name)
     x = synth.make_batch(cfg, seed=0)
     rows = mpm.local_block_rows(cfg.B, cfg.N, cfg.D, x.dtype, cfg.G, window)
-    print(f"local schedule {name} window={window}: B={cfg.B} N={cfg.N} D={cfg.D}, {rows}-row blocks", flush=True)
-    res = mpm.run_schedule(x.to(DEV), insertions=cfg.insertions, grid_w=cfg.G, window=window)
+    block_rows = (384 - rows) if forced else 0   # the other of 128 and 256
+    if forced:
+        rows = block_rows
+    else:
+        images = range(cfg.B)
+    print(f"local schedule {name} window={window}: B={cfg.B} N={cfg.N} D={cfg.D}, {rows}-row blocks"
+          f"{' (forced)' if forced else ''}, images checked: {len(images)}", flush=True)
+    res = mpm.run_schedule(x.to(DEV), insertions=cfg.insertions, grid_w=cfg.G, window=window, block_rows=block_rows)
     torch.cuda.synchronize()
     flips = sum(check_local_schedule_image(x[b], cfg.dtype, res, b, cfg.G, window) for b in images)
     counts = [torch.diff(st.y_off.cpu()).tolist() for st in res.stages]
