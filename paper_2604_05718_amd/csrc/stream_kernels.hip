@@ -25,6 +25,8 @@ constexpr int kGatherBatch = 4;
 constexpr int kAverageBatch = 2;  // each vector of the average already loads two rows
 constexpr int kMaxRowsPerBlock = 4096;       // rows one gather workgroup resolves into LDS (16 KB)
 constexpr int kInvBatch = 8;  // vectors per lane at most, in the pair average that also writes row norms
+constexpr int kXcdCount = 8;                    // MI355X: workgroups are dealt round-robin to 8 XCDs
+constexpr long kXcdL2Bytes = 4L << 20;          // ... each with a 4 MB L2
 
 // Lanes per row in the pair average that also writes row norms: a power of two, at
 // most a wave, enough for at most kInvBatch vectors per lane where a wave allows it.
@@ -227,12 +229,23 @@ template <class S>
 __global__ __launch_bounds__(kRowThreads) void unmerge_kernel(
     const uint8_t* __restrict__ z, const int32_t* __restrict__ z_off, const int32_t* __restrict__ map,
     const int32_t* __restrict__ map2, int32_t* __restrict__ map_ab, const uint8_t* __restrict__ z_spec, int E,
-    int N, int D, int rows_per_block, uint8_t* __restrict__ out)
+    int N, int D, int rows_per_block, uint8_t* __restrict__ out, int B, int xcd_major)
 {
     __shared__ int32_t src_row[kMaxRowsPerBlock];
-    const int b = blockIdx.y;
+    // Row block and image of this workgroup: (blockIdx.x, blockIdx.y), or, XCD-major (a
+    // one-dimensional grid; workgroup L runs on XCD L % 8), every row block of an image on
+    // one XCD, so the merged rows two row blocks share (a pair's tokens a grid row apart)
+    // are read through one L2.
+    int b = blockIdx.y, xb = blockIdx.x;
+    if (xcd_major) {
+        const int nx = (E + N + rows_per_block - 1) / rows_per_block;
+        const int k = blockIdx.x / kXcdCount;
+        b = blockIdx.x % kXcdCount + kXcdCount * (k / nx);
+        xb = k % nx;
+        if (b >= B) return;
+    }
     const int rows = E + N;
-    const int r0 = blockIdx.x * rows_per_block;
+    const int r0 = xb * rows_per_block;
     const int r1 = min(rows, r0 + rows_per_block);
     if (r0 >= r1) return;
     const long rowbytes = (long)D * S::kBytes;
@@ -351,16 +364,20 @@ hipError_t launch_unmerge(const void* z, const int32_t* z_off, const int32_t* ma
 {
     const long rowbytes = (long)D * (dt == kBf16 ? 2 : 4);
     const int rpb = rows_per_block_for(rowbytes, kGatherBytesPerBlock);
-    dim3 grid((E + N + rpb - 1) / rpb, B);
+    const int nx = (E + N + rpb - 1) / rpb;
+    // XCD-major where a batch covers every XCD and an image's rows fit in one XCD's L2.
+    const bool xcd_major = B >= kXcdCount && (long)N * rowbytes <= kXcdL2Bytes;
+    const dim3 grid = xcd_major ? dim3((unsigned)((long)nx * ((B + kXcdCount - 1) / kXcdCount) * kXcdCount), 1)
+                                : dim3((unsigned)nx, (unsigned)B);
     const uint8_t* zp = static_cast<const uint8_t*>(z);
     const uint8_t* sp = static_cast<const uint8_t*>(z_spec);
     uint8_t* op = static_cast<uint8_t*>(out);
     if (dt == kBf16)
         hipLaunchKernelGGL(unmerge_kernel<Bf16>, grid, dim3(kRowThreads), 0, stream, zp, z_off, map, map2, map_ab, sp, E,
-                           N, D, rpb, op);
+                           N, D, rpb, op, B, xcd_major ? 1 : 0);
     else
         hipLaunchKernelGGL(unmerge_kernel<F32>, grid, dim3(kRowThreads), 0, stream, zp, z_off, map, map2, map_ab, sp, E,
-                           N, D, rpb, op);
+                           N, D, rpb, op, B, xcd_major ? 1 : 0);
     return hipGetLastError();
 }
 
