@@ -47,8 +47,9 @@
  *   Device-side faults surface at the caller's next synchronisation.
  * - Results are deterministic: the same inputs give bitwise-identical outputs.
  * - Reentrant: no mutable global state besides the per-thread last HIP error
- *   and, for mpm_merge_noalloc, the device address of its array per GPU (set
- *   once). Calls that share a workspace must be ordered (one stream, or events).
+ *   and, for mpm_merge_noalloc and the checked mode below, the device address of
+ *   a library array per GPU (set once). Calls that share a workspace must be
+ *   ordered (one stream, or events).
  * - Fault injection: with MPM_FAULT_INJECT=launch in the environment (read once,
  *   at the first call), every entry point that would launch a kernel returns
  *   MPM_ERR_HIP with hipErrorLaunchFailure recorded, after its argument checks and
