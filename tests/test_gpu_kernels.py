@@ -241,18 +241,20 @@ def test_compose_and_unmerge_with_special_rows():
             assert np.array_equal(got[E + i], want)
 
 
+@pytest.mark.parametrize("B", [4, 9])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("packed,E", [(True, 2), (False, 0), (True, 0)])
-def test_compose_unmerge_matches_compose_then_unmerge(dtype, packed, E):
+def test_compose_unmerge_matches_compose_then_unmerge(dtype, packed, E, B):
     """mpm_compose_unmerge (Eq. 3 folded into Eq. 4) equals mpm_compose followed by
-    mpm_unmerge bit for bit, against the oracle's composition, and works with the
-    composed-map output omitted (NULL)."""
+    mpm_unmerge bit for bit, and a host gather through the oracle's composition; it
+    works with the composed-map output omitted (NULL). Nine images take the gather's
+    XCD-major workgroup order, four the plain one."""
     from paper_2604_05718_amd import _lib, api
 
     rng = np.random.default_rng(11)
-    B, N, D = 4, 200, 40
-    n1s = [150, 200, 1, 97]
-    n2s = [110, 133, 1, 60]
+    N, D = 200, 40
+    n1s = [150, 200, 1, 97, 200, 3, 64, 120, 2][:B]
+    n2s = [110, 133, 1, 60, 100, 2, 33, 61, 1][:B]
     r1 = np.full((B, N), -1, np.int32)
     r2 = np.full((B, N), -1, np.int32)
     for b in range(B):
@@ -282,8 +284,18 @@ def test_compose_unmerge_matches_compose_then_unmerge(dtype, packed, E):
     assert torch.equal(out, ref)
     assert torch.equal(out2, ref)
     rs = rstar.cpu().numpy()
+    zc = z.float().cpu().numpy()
+    oc = out.float().cpu().numpy()
+    sc = spec.float().cpu().numpy() if E else None
+    zo = np.concatenate([[0], np.cumsum(n2s)]) if packed else np.arange(B + 1) * N
     for b in range(B):
         assert np.array_equal(rs[b], oracle.compose(r1[b], r2[b]))
+        want = np.zeros((E + N, D))
+        if E:
+            want[:E] = sc[b]
+        live = rs[b] >= 0
+        want[E:][live] = zc[zo[b] + rs[b][live]]
+        assert np.array_equal(oc[b], want), b
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
