@@ -34,8 +34,8 @@ METRIC = "MPM merge+unmerge images/s at ViT-B N=1024 B=64; % MFMA and % HBM peak
 # kernel (profiles/<workload>_rocprof.md). Valid only for the kernel source it was
 # measured on, with the default schedule.
 TRAFFIC = {"source_sha256": "1dae8e815f91dc3ce104e116133adef4251abc9e32c244ab1520b8269f69403b",
-           "bytes_per_launch": {"vit_ti_512": 6556908, "vit_s_512": 25826093, "vit_b_512": 151371046,
-                                "vit_l_1024": 510609428, "stress_768": 181822003}}
+           "bytes_per_launch": {"vit_ti_512": 6556918, "vit_s_512": 25826114, "vit_b_512": 151363482,
+                                "vit_l_1024": 510513327, "stress_768": 182216409}}
 
 
 def log(*a):
