@@ -124,11 +124,13 @@ def test_local_schedule_random_grids(dtype, gh, gw, D, window, B, block_rows):
 @pytest.mark.timeout(900)
 @pytest.mark.parametrize("forced", [False, True])
 @pytest.mark.parametrize("name,window,images", [("vit_b_512", 3, [0, 21, 63]), ("vit_l_1024", 4, [0, 9, 15]),
-                                                 ("stress_768", 4, [0, 5, 31])])
+                                                 ("stress_768", 4, [0, 5, 31]), ("vit_s_512", 2, [0, 31]),
+                                                 ("vit_ti_512", 2, [0])])
 def test_local_schedule_full_size(name, window, images, forced):
-    """The windowed schedule on a full benchmark batch: with the block size the library
-    picks (the launch configuration bench.py --window times), every image checked
-    completely; with the other block size forced, sampled images."""
+    """The windowed schedule on a full benchmark batch (ViT-Ti: one float32 image, a
+    single insertion): with the block size the library picks (the launch configuration
+    bench.py --window times), every image checked completely; with the other block size
+    forced, sampled images."""
     cfg = synth.config(name)
     x = synth.make_batch(cfg, seed=0)
     rows = mpm.local_block_rows(cfg.B, cfg.N, cfg.D, x.dtype, cfg.G, window)
