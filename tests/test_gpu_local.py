@@ -148,6 +148,20 @@ def test_local_schedule_full_size(name, window, images, forced):
     print(f"  survivors (mean): {[round(sum(c) / len(c), 1) for c in counts]}, accepted flips {flips}", flush=True)
 
 
+@pytest.mark.parametrize("seed", [1, 2])
+@pytest.mark.parametrize("name,window", [("vit_b_512", 3), ("stress_768", 4), ("vit_l_1024", 4)])
+def test_local_schedule_other_seeds(name, window, seed):
+    """The windowed schedule on full batches drawn with seeds 1 and 2 (the picked block
+    size), the first, a middle and the last image checked completely."""
+    cfg = synth.config(name)
+    x = synth.make_batch(cfg, seed=seed)
+    print(f"local schedule {name} window={window} seed={seed}", flush=True)
+    res = mpm.run_schedule(x.to(DEV), insertions=cfg.insertions, grid_w=cfg.G, window=window)
+    torch.cuda.synchronize()
+    for b in sorted({0, cfg.B // 2, cfg.B - 1}):
+        check_local_schedule_image(x[b], cfg.dtype, res, b, cfg.G, window)
+
+
 @pytest.mark.parametrize("block_rows", [128, 256])
 @pytest.mark.parametrize("dtype,given_norms", [("f32", False), ("bf16", False), ("bf16", True)])
 @pytest.mark.parametrize("given_pos", [False, True])
