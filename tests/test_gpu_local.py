@@ -148,6 +148,22 @@ def test_local_schedule_full_size(name, window, images, forced):
     print(f"  survivors (mean): {[round(sum(c) / len(c), 1) for c in counts]}, accepted flips {flips}", flush=True)
 
 
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("block_rows", [128, 256])
+def test_local_schedule_max_size(block_rows):
+    """The largest image the ABI accepts (N = 16384, a 128 x 128 grid: 128 or 64 square
+    blocks, as many partial slots per token to reduce), window 2, two insertions."""
+    rng = np.random.default_rng(16384)
+    G, D = 128, 64
+    cent = rng.standard_normal((40, D))
+    lab = rng.integers(0, 40, G * G)
+    x = store(cent[lab] + 0.3 * rng.standard_normal((G * G, D)), "bf16")[None]
+    print(f"local schedule max size N={G * G} blocks {block_rows}", flush=True)
+    res = mpm.run_schedule(x.to(DEV), insertions=2, grid_w=G, window=2, block_rows=block_rows)
+    torch.cuda.synchronize()
+    check_local_schedule_image(x[0], "bf16", res, 0, G, 2)
+
+
 @pytest.mark.parametrize("seed", [1, 2])
 @pytest.mark.parametrize("name,window", [("vit_b_512", 3), ("stress_768", 4), ("vit_l_1024", 4)])
 def test_local_schedule_other_seeds(name, window, seed):
