@@ -745,6 +745,27 @@ def test_many_images():
         assert rel_err(y[y_off[b]:y_off[b + 1]], ref.y) <= 2e-2, b
 
 
+def test_maximum_images():
+    """B = MPM_MAX_B images of 5 tokens (64-byte rows): two insertions (the second on
+    ragged packed survivors, with the norms the first wrote), composition and gather,
+    every image checked stage by stage and end to end against the oracle. The
+    compaction's arrival counter then counts the whole sync region's images, and
+    every per-image grid is at its largest."""
+    from parity import to_host
+    rng = np.random.default_rng(65535)
+    B, N, D = 65535, 5, 32
+    x = store(rng.standard_normal((B * N, D)), "bf16").view(B, N, D)
+    print(f"maximum images: B={B} N={N} D={D} bf16, two insertions", flush=True)
+    res = mpm.run_schedule(x.to(DEV), insertions=2)
+    torch.cuda.synchronize()
+    h = to_host(res)
+    flips = 0
+    for b in range(B):
+        reps = check_schedule_image(x[b], "bf16", h, b, threads=1)
+        flips += sum(r.flipped_rows for r in reps)
+    print(f"  {B} images checked, {flips} accepted near-tie flips", flush=True)
+
+
 # ---- the affinity + compaction step ----------------------------------------------------
 
 def _step_case(name):
