@@ -150,7 +150,7 @@ def cpu_baseline(cfg, x_cpu, budget_s: float, threads: int | None = None):
 
 
 def backbone(args, cfg, dev) -> int:
-    """The paper's end-to-end setting on this build: a ViT encoder (random weights, 12
+    """The paper's end-to-end setting with this library's kernels: a ViT encoder (random weights, 12
     blocks, the workload's width, 64-wide heads) with MPM before blocks 2 and 5 and the
     gather after the last block, against the same encoder without merging; whole
     forward passes timed, images/s for both."""
@@ -251,7 +251,7 @@ def main() -> int:
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        log("bench.py: this build measures one GPU only; the path shards by image with no communication, "
+        log("bench.py: measures one GPU only; the path shards by image with no communication, "
             "so a multi-GPU figure is not produced. Run with --gpus 1.")
         return 2
 
