@@ -37,8 +37,8 @@ AFFINITY_REPS = 5    # such batches per insertion; the median is taken
 # kernel (profiles/<workload>_rocprof.md). Valid only for the kernel source it was
 # measured on, with the default schedule.
 TRAFFIC = {"source_sha256": "1dae8e815f91dc3ce104e116133adef4251abc9e32c244ab1520b8269f69403b",
-           "bytes_per_launch": {"vit_ti_512": 6556918, "vit_s_512": 25826114, "vit_b_512": 151363482,
-                                "vit_l_1024": 510513327, "stress_768": 182216409}}
+           "bytes_per_launch": {"vit_ti_512": 6556890, "vit_s_512": 25826025, "vit_b_512": 151433431,
+                                "vit_l_1024": 510617954, "stress_768": 182226447}}
 
 
 def log(*a):
