@@ -27,9 +27,10 @@
  * - A batch holds B images of at most N tokens each. Token rows are either
  *   DENSE (offsets pointer NULL: image b owns rows [b*N, b*N + N)) or PACKED
  *   (offsets pointer = device int32[B+1], image b owns rows
- *   [off[b], off[b+1]), n_b = off[b+1] - off[b] with 1 <= n_b <= N, offsets
- *   non-decreasing). Packed offsets are data on the device; violating these
- *   rules is undefined behaviour, not a reported error.
+ *   [off[b], off[b+1]), n_b = off[b+1] - off[b] with 0 <= n_b <= N, offsets
+ *   non-decreasing). An empty image (n_b = 0) gets no merged rows and a map of
+ *   -1. Packed offsets are data on the device; violating these rules is
+ *   undefined behaviour, not a reported error.
  * - Per-token integer arrays (nb, map) use a [B][N] slot layout: entry
  *   b*N + i belongs to token i of image b, for i < n_b. Ids are 0-based and
  *   image-local.
@@ -57,8 +58,8 @@
  * - Checked mode (debugging): with MPM_CHECKED=1 in the environment (read once, at
  *   the first call), every entry point also validates on the device the data
  *   preconditions that are otherwise undefined behaviour, before launching its
- *   operation: packed offsets (1 <= n_b <= N; merged-row offsets also at most the
- *   tokens they come from, within B*N rows; the padded layout's at most P), token
+ *   operation: packed offsets (0 <= n_b <= N; merged-row offsets also at most the
+ *   tokens they come from, within B*N rows; the padded layout's any n_b >= 0), token
  *   values and given inverse norms (finite; norms positive), grid positions (in
  *   range, rows non-decreasing), neighbours (in [0, n_b), not the token itself, -1
  *   for a one-token image), merged-row sources (in [0, n_b)) and maps (in [-1, N),

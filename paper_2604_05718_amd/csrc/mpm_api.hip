@@ -96,7 +96,7 @@ int run_checks(hipStream_t st, F&& launch_checks)
     return host == 0 ? MPM_OK : MPM_ERR_INVALID_ARG;
 }
 
-// Packed offsets of the rows of x (1 <= n_b <= N), then the rows themselves (finite),
+// Packed offsets of the rows of x (0 <= n_b <= N), then the rows themselves (finite),
 // their given inverse norms (finite, positive) and grid positions (in range, rows
 // non-decreasing), each where given.
 int checked_rows(const void* x, const int32_t* x_off, const float* x_inv, const int32_t* pos, int grid_w, int32_t B,
@@ -105,7 +105,7 @@ int checked_rows(const void* x, const int32_t* x_off, const float* x_inv, const 
     std::lock_guard<std::mutex> lock(g_check_mutex);
     int s = MPM_OK;
     if (x_off)
-        s = run_checks(st, [&](int32_t* v) { return mpm::launch_check_offsets(x_off, B, N, 1, -1, nullptr, v, st); });
+        s = run_checks(st, [&](int32_t* v) { return mpm::launch_check_offsets(x_off, B, N, 0, -1, nullptr, v, st); });
     if (s != MPM_OK) return s;
     return run_checks(st, [&](int32_t* v) {
         hipError_t e = mpm::launch_check_finite(x, x_off, B, N, D, dt, v, st);
@@ -125,8 +125,8 @@ int checked_pairs(const int32_t* x_off, const int32_t* nb, const int32_t* y_off,
     std::lock_guard<std::mutex> lock(g_check_mutex);
     int s = run_checks(st, [&](int32_t* v) {
         hipError_t e = hipSuccess;
-        if (x_off) e = mpm::launch_check_offsets(x_off, B, N, 1, -1, nullptr, v, st);
-        if (e == hipSuccess && y_off) e = mpm::launch_check_offsets(y_off, B, N, 1, (long)B * N, x_off, v, st);
+        if (x_off) e = mpm::launch_check_offsets(x_off, B, N, 0, -1, nullptr, v, st);
+        if (e == hipSuccess && y_off) e = mpm::launch_check_offsets(y_off, B, N, 0, (long)B * N, x_off, v, st);
         return e;
     });
     if (s != MPM_OK) return s;
@@ -136,16 +136,16 @@ int checked_pairs(const int32_t* x_off, const int32_t* nb, const int32_t* y_off,
     });
 }
 
-// Offsets of the merged rows z (where given; P rows per image at most for the padded
-// layout), then maps: map_a in [-1, N) (it indexes map_b's slots, or z's rows when
-// map_b is null) and map_b in [-1, n_z).
+// Offsets of the merged rows z (where given; at most rows_max rows per image), then
+// maps: map_a in [-1, N) (it indexes map_b's slots, or z's rows when map_b is null) and
+// map_b in [-1, n_z).
 int checked_maps(const int32_t* z_off, int32_t rows_max, const int32_t* map_a, const int32_t* map_b, int32_t B,
                  int32_t N, hipStream_t st)
 {
     std::lock_guard<std::mutex> lock(g_check_mutex);
     int s = MPM_OK;
     if (z_off)
-        s = run_checks(st, [&](int32_t* v) { return mpm::launch_check_offsets(z_off, B, rows_max, 1, -1, nullptr, v, st); });
+        s = run_checks(st, [&](int32_t* v) { return mpm::launch_check_offsets(z_off, B, rows_max, 0, -1, nullptr, v, st); });
     if (s != MPM_OK || map_a == nullptr) return s;
     return run_checks(st, [&](int32_t* v) {
         hipError_t e = mpm::launch_check_slots(map_a, 1, nullptr, -1, map_b ? nullptr : z_off, B, N,
@@ -543,7 +543,7 @@ int mpm_pad(const void* z, const int32_t* z_off, int32_t B, int32_t P, int32_t r
     if (B > MPM_MAX_B || P > MPM_MAX_N || row_bytes > MPM_MAX_D * 4) return MPM_ERR_UNSUPPORTED;
     if (!ok_rows_ptr(z) || !ok_int_ptr(z_off) || !ok_rows_ptr(out)) return MPM_ERR_INVALID_ARG;
     MPM_LAUNCH_GATE();
-    MPM_DATA_CHECK(checked_maps(z_off, P, nullptr, nullptr, B, P, as_stream(stream)));
+    MPM_DATA_CHECK(checked_maps(z_off, INT32_MAX, nullptr, nullptr, B, P, as_stream(stream)));
     return hip_status(mpm::launch_pad(z, z_off, B, P, row_bytes, out, false, as_stream(stream)));
 }
 
@@ -554,7 +554,7 @@ int mpm_unpad(const void* padded, const int32_t* z_off, int32_t B, int32_t P, in
     if (B > MPM_MAX_B || P > MPM_MAX_N || row_bytes > MPM_MAX_D * 4) return MPM_ERR_UNSUPPORTED;
     if (!ok_rows_ptr(padded) || !ok_int_ptr(z_off) || !ok_rows_ptr(z)) return MPM_ERR_INVALID_ARG;
     MPM_LAUNCH_GATE();
-    MPM_DATA_CHECK(checked_maps(z_off, P, nullptr, nullptr, B, P, as_stream(stream)));
+    MPM_DATA_CHECK(checked_maps(z_off, INT32_MAX, nullptr, nullptr, B, P, as_stream(stream)));
     return hip_status(mpm::launch_pad(padded, z_off, B, P, row_bytes, z, true, as_stream(stream)));
 }
 

@@ -60,9 +60,13 @@ def untouched(y_off, m):
     return bool((y_off.cpu() == -7).all() and (m.cpu() == -7).all())
 
 for name, bad in [("count_above_N", [0, 301, 478, 479]), ("decreasing", [0, 300, 200, 479]),
-                  ("negative_start", [-1, 299, 476, 477]), ("empty_image", [0, 300, 300, 301])]:
+                  ("negative_start", [-1, 299, 476, 477])]:
     rc, y2, yo2, m2 = merge(x, torch.tensor(bad, dtype=torch.int32, device=dev))
     results["offsets_" + name] = [rc, untouched(yo2, m2)]
+# An empty image is valid: no merged rows, a map of -1.
+rc, y2, yo2, m2 = merge(x, torch.tensor([0, 300, 300, 301], dtype=torch.int32, device=dev))
+yo2 = yo2.cpu().tolist()
+results["empty_image"] = [rc, yo2[2] == yo2[1] and yo2[3] == yo2[2] + 1 and bool((m2[1].cpu() == -1).all())]
 xn = x.clone()
 xn[200, 5] = float("nan")
 rc, _, yo2, m2 = merge(xn, x_off)
@@ -153,7 +157,11 @@ results["unmerge_bad_offsets"] = list(unmerge(mu, torch.tensor([0, 10, 5, 21], d
 # padded layout
 out = torch.zeros((B, 12, D), dtype=torch.bfloat16, device=dev)
 results["pad_valid"] = lib.mpm_pad(P(z), P(z_off), B, 12, D * 2, P(out), st)
-results["pad_too_long"] = lib.mpm_pad(P(z), P(z_off), B, 9, D * 2, P(out), st)
+results["pad_rows_past_P"] = lib.mpm_pad(P(z), P(z_off), B, 9, D * 2, P(out), st)  # rows past P are dropped
+results["pad_empty_image"] = lib.mpm_pad(P(z), P(torch.tensor([0, 10, 10, 21], dtype=torch.int32, device=dev)), B,
+                                         12, D * 2, P(out), st)
+results["pad_bad_offsets"] = lib.mpm_pad(P(z), P(torch.tensor([0, 10, 5, 21], dtype=torch.int32, device=dev)), B,
+                                         12, D * 2, P(out), st)
 torch.cuda.synchronize()
 print("RESULTS " + json.dumps(results), flush=True)
 """
@@ -171,14 +179,15 @@ def test_checked_mode(tmp_path):
     r = json.loads(line[len("RESULTS "):])
     ok, bad = 0, 1
     for key in ("valid_merge", "valid_norms", "local_valid", "compact_valid", "average_valid", "compose_valid",
-                "unmerge_valid", "pad_valid"):
+                "unmerge_valid", "pad_valid", "pad_rows_past_P", "pad_empty_image"):
         assert r[key] == ok, (key, r[key])
-    for key in ("offsets_count_above_N", "offsets_decreasing", "offsets_negative_start", "offsets_empty_image",
+    assert r["empty_image"] == [ok, True]
+    for key in ("offsets_count_above_N", "offsets_decreasing", "offsets_negative_start",
                 "nan_token", "norms_zero", "norms_negative", "norms_inf", "local_row_back", "local_negative",
                 "compact_nb_out_of_range", "compact_nb_self", "compact_nb_single", "average_src_out_of_range",
                 "average_too_many_rows", "compose_out_of_range", "unmerge_out_of_range", "unmerge_bad_offsets"):
         assert r[key] == [bad, True], (key, r[key])   # rejected, outputs untouched
-    assert r["pad_too_long"] == bad
+    assert r["pad_bad_offsets"] == bad
 
     # The checked valid merge equals this process's unchecked one, bit for bit.
     got = np.load(saved)

@@ -766,6 +766,60 @@ def test_maximum_images():
     print(f"  {B} images checked, {flips} accepted near-tie flips", flush=True)
 
 
+# ---- empty images in a packed batch --------------------------------------------------
+
+_EMPTY_SIZES = [0, 5, 0, 300, 1, 0, 257, 2, 0, 600]
+EMPTY_CASES = {  # (D, dtype, schedule, image sizes)
+    "persistent_bf16": (64, "bf16", "auto", _EMPTY_SIZES),
+    "persistent_bf16_full": (64, "bf16", "full", _EMPTY_SIZES),
+    "persistent_bf16_symmetric": (64, "bf16", "symmetric", _EMPTY_SIZES),
+    "persistent_f32": (32, "f32", "auto", _EMPTY_SIZES),
+    "staged_bf16": (24, "bf16", "auto", _EMPTY_SIZES),                   # 48-byte rows
+    "small_blocks": (64, "bf16", "full_64", [0, 700, 0]),
+    "symmetric_deferred": (64, "bf16", "symmetric", [0, 1024, 700, 0, 1, 1024] * 15),  # the half-block launch
+}
+
+
+@pytest.mark.parametrize("case", list(EMPTY_CASES))
+def test_empty_images(case):
+    """Packed batches with empty images (n_b = 0) between ragged ones: two insertions
+    (the second on the first's packed output), composition and gather. An empty image
+    gets no merged rows, a map of -1 and zero rows from the gather; the others match
+    the oracle stage by stage and through the reconstruction."""
+    D, dtype, schedule, ns = EMPTY_CASES[case]
+    rng = np.random.default_rng(zlib.crc32(("empty-" + case).encode()))
+    N = max(ns)
+    imgs = [store(clustered(rng, n, D, k=max(1, n // 8)), dtype) for n in ns]
+    x = torch.cat(imgs).to(DEV)
+    off = torch.tensor(np.concatenate([[0], np.cumsum(ns)]), dtype=torch.int32, device=DEV)
+    print(f"empty images {case}: {len(ns)} images, sizes {sorted(set(ns))}, D={D} {dtype} schedule={schedule}",
+          flush=True)
+    m1 = mpm.merge(x, off, N=N, schedule=schedule)
+    m2 = mpm.merge(m1.y, m1.y_off, N=N, schedule=schedule)
+    out, rstar = mpm.compose_unmerge(m2.y, m2.y_off, m1.map, m2.map)
+    torch.cuda.synchronize()
+    o1, o2 = m1.y_off.cpu().numpy(), m2.y_off.cpu().numpy()
+    nb1, nb2 = m1.nb.cpu().numpy(), m2.nb.cpu().numpy()
+    map1, map2, rs = m1.map.cpu().numpy(), m2.map.cpu().numpy(), rstar.cpu().numpy()
+    y1, y2 = to64(m1.y[: o1[-1]]), to64(m2.y[: o2[-1]])
+    up = to64(out)
+    for b, n in enumerate(ns):
+        if n == 0:
+            assert o1[b + 1] == o1[b] and o2[b + 1] == o2[b], f"image {b}: merged rows of an empty image"
+            assert np.all(map1[b] == -1) and np.all(map2[b] == -1) and np.all(rs[b] == -1), f"image {b}: maps"
+            assert not up[b].any(), f"image {b}: gather of an empty image"
+            continue
+        x0 = to64(imgs[b])
+        s1 = check_stage(x0, dtype, nb1[b, :n], map1[b], y1[o1[b]:o1[b + 1]])
+        n1 = s1.count
+        s2 = check_stage(y1[o1[b]:o1[b + 1]], dtype, nb2[b, :n1], map2[b], y2[o2[b]:o2[b + 1]])
+        r = oracle.compose(map1[b, :n], map2[b, :n1])
+        assert np.array_equal(rs[b, :n], r) and np.all(rs[b, n:] == -1), f"image {b}: composed map"
+        assert np.array_equal(up[b, :n], oracle.unmerge(y2[o2[b]:o2[b + 1]], r)), f"image {b}: gather"
+        assert not up[b, n:].any(), f"image {b}: rows past n_b"
+        assert s2.count <= n1 <= n
+
+
 # ---- the affinity + compaction step ----------------------------------------------------
 
 def _step_case(name):
