@@ -797,7 +797,15 @@ def test_empty_images(case):
     m1 = mpm.merge(x, off, N=N, schedule=schedule)
     m2 = mpm.merge(m1.y, m1.y_off, N=N, schedule=schedule)
     out, rstar = mpm.compose_unmerge(m2.y, m2.y_off, m1.map, m2.map)
+    # The step entry points on the same batch: neighbours, then the compaction from them.
+    nb_step = mpm.argmax(x, off, N=N, schedule=schedule)
+    map_step, src_step, yoff_step = mpm.pair_compact(nb_step, off)
     torch.cuda.synchronize()
+    assert torch.equal(yoff_step, m1.y_off)
+    for b, n in enumerate(ns):
+        assert torch.equal(nb_step[b, :n], m1.nb[b, :n]) and torch.equal(map_step[b], m1.map[b]), f"image {b}"
+        c = int(m1.y_off[b + 1] - m1.y_off[b])
+        assert torch.equal(src_step[b, :c], m1.src[b, :c]), f"image {b}: sources"
     o1, o2 = m1.y_off.cpu().numpy(), m2.y_off.cpu().numpy()
     nb1, nb2 = m1.nb.cpu().numpy(), m2.nb.cpu().numpy()
     map1, map2, rs = m1.map.cpu().numpy(), m2.map.cpu().numpy(), rstar.cpu().numpy()
