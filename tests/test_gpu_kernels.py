@@ -766,6 +766,43 @@ def test_maximum_images():
     print(f"  {B} images checked, {flips} accepted near-tie flips", flush=True)
 
 
+def test_workspace_sync_region_left_zero():
+    """Every call leaves the workspace's arrival counters (the sync region, MPM_MAX_B + 1
+    words at its start) zero, so one workspace serves any sequence of calls: dense and
+    packed merges, the windowed merge, the fused affinity + compaction step, a batch at
+    MPM_MAX_B, and a merge after a smaller one in the same workspace."""
+    from paper_2604_05718_amd import _lib
+    rng = np.random.default_rng(4)
+    sync_words = 65536
+
+    def sync_zero(ws):
+        torch.cuda.synchronize()
+        off = _lib.workspace_offsets(1, 1)["sync"]
+        return int(ws[off:off + 4 * sync_words].view(torch.int32).abs().sum()) == 0
+
+    x = store(rng.standard_normal((9 * 300, 64)), "bf16").view(9, 300, 64).to(DEV)
+    ws = mpm.new_workspace(9, 300, DEV)
+    assert sync_zero(ws)
+    mpm.merge(x, ws=ws)
+    assert sync_zero(ws), "dense merge"
+    ns = [300, 0, 17, 1, 256, 299, 2, 64, 5]
+    off = torch.tensor(np.concatenate([[0], np.cumsum(ns)]), dtype=torch.int32, device=DEV)
+    xp = x.view(-1, 64)[: sum(ns)].contiguous()
+    mpm.merge(xp, off, N=300, ws=ws, schedule="symmetric")
+    assert sync_zero(ws), "packed merge"
+    mpm.merge_local(x, 20, 2, ws=ws)
+    assert sync_zero(ws), "windowed merge"
+    mpm.insertion(x, ws=ws)
+    assert sync_zero(ws), "affinity + compaction"
+    mpm.merge(x[:3].contiguous(), ws=ws)
+    mpm.merge(x, ws=ws)
+    assert sync_zero(ws), "smaller batch, then the full one"
+    xb = store(rng.standard_normal((65535 * 3, 32)), "bf16").view(65535, 3, 32).to(DEV)
+    wsb = mpm.new_workspace(65535, 3, DEV)
+    mpm.merge(xb, ws=wsb)
+    assert sync_zero(wsb), "MPM_MAX_B images"
+
+
 # ---- empty images in a packed batch --------------------------------------------------
 
 _EMPTY_SIZES = [0, 5, 0, 300, 1, 0, 257, 2, 0, 600]
