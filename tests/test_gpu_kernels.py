@@ -803,6 +803,56 @@ def test_workspace_sync_region_left_zero():
     assert sync_zero(wsb), "MPM_MAX_B images"
 
 
+def test_concurrent_calls_on_two_streams():
+    """Two host threads, each on a stream of its own with its own workspace, merge
+    different batches (dense bfloat16 under the symmetric schedule; packed ragged
+    float32 under the full one) 20 times each, their launches interleaved on the
+    device. Every result equals the same call made alone: the library keeps no state
+    between calls beyond the caller's workspace."""
+    import threading
+    rng = np.random.default_rng(8)
+    xa = torch.stack([store(clustered(rng, 1024, 128, k=40), "bf16") for _ in range(16)]).to(DEV)
+    ns = [700, 1, 333, 0, 512, 699, 2]
+    xb = store(clustered(rng, sum(ns), 64, k=50), "f32").to(DEV)
+    offb = torch.tensor(np.concatenate([[0], np.cumsum(ns)]), dtype=torch.int32, device=DEV)
+    calls = [lambda ws: mpm.merge(xa, ws=ws, schedule="symmetric"),
+             lambda ws: mpm.merge(xb, offb, N=700, ws=ws, schedule="full")]
+    want = []
+    for call in calls:
+        m = call(None)
+        torch.cuda.synchronize()
+        want.append((m.y_off.clone(), m.map.clone(), m.y[: int(m.y_off[-1])].clone()))
+    print("concurrent: two threads, two streams, 20 merges each", flush=True)
+    got, errors = [[], []], []
+
+    def worker(t):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                ws = mpm.new_workspace(16, 1024, DEV)
+                for _ in range(20):
+                    m = calls[t](ws)
+                    got[t].append((m.y_off, m.map, m.y))
+            s.synchronize()
+        except Exception as exc:  # re-raised by the main thread
+            errors.append(exc)
+
+    threads = [threading.Thread(target=worker, args=(t,)) for t in range(2)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for t in range(2):
+        y_off, m, y = want[t]
+        assert len(got[t]) == 20
+        for k, (go, gm, gy) in enumerate(got[t]):
+            assert torch.equal(go, y_off) and torch.equal(gm, m), (t, k)
+            assert torch.equal(gy[: y.shape[0]].view(torch.int16 if y.dtype == torch.bfloat16 else torch.int32),
+                               y.view(torch.int16 if y.dtype == torch.bfloat16 else torch.int32)), (t, k)
+
+
 # ---- empty images in a packed batch --------------------------------------------------
 
 _EMPTY_SIZES = [0, 5, 0, 300, 1, 0, 257, 2, 0, 600]
