@@ -418,16 +418,18 @@ def test_timed_schedule_equals_untimed():
         assert 0.0 < ms < 1000.0
 
 
-def test_graph_replay_matches_eager():
-    """The schedule captured once in a HIP graph and replayed several times, with
-    eager kernels touching its outputs in between, reproduces the eager results
-    bit for bit on every replay (no memset nodes are captured)."""
+@pytest.mark.parametrize("window", [None, 2])
+def test_graph_replay_matches_eager(window):
+    """The schedule (dense, or locality-constrained on a 20-column grid) captured once
+    in a HIP graph and replayed several times, with eager kernels touching its outputs
+    in between, reproduces the eager results bit for bit on every replay (no memset
+    nodes are captured)."""
     from paper_2604_05718_amd import api
 
     rng = np.random.default_rng(23)
     B, N, D = 9, 600, 192
     x = torch.stack([store(clustered(rng, N, D, k=15, sigma=0.3), "bf16") for _ in range(B)]).to(DEV)
-    sched = api.Schedule(B, N, D, torch.bfloat16, insertions=2)
+    sched = api.Schedule(B, N, D, torch.bfloat16, insertions=2, grid_w=None if window is None else 20, window=window)
     ref_out = sched.run(x).clone()
     ref_rstar = sched.rstar.clone()
     ref_maps = [m.clone() for m in sched.map]
