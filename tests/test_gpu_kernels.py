@@ -855,6 +855,57 @@ def test_concurrent_calls_on_two_streams():
                                y.view(torch.int16 if y.dtype == torch.bfloat16 else torch.int32)), (t, k)
 
 
+def _random_config(seed):
+    """A seeded configuration across the shape space: 1-8 images of up to 1100 tokens
+    (dense, or packed with ragged and empty images), rows of 16 bytes to about 2 KB in
+    either dtype, any schedule, two insertions."""
+    rng = np.random.default_rng(1000 + seed)
+    dtype = ["f32", "bf16"][rng.integers(0, 2)]
+    unit = 4 if dtype == "f32" else 8
+    D = int(unit * rng.integers(1, 1040 // (unit * 2) + 1))
+    B = int(rng.integers(1, 9))
+    N = int(rng.choice([1, 2, 31, 64, 255, 256, 257, 513, 777, 1024, 1100]))
+    packed = bool(rng.integers(0, 2))
+    ns = [int(rng.integers(0, N + 1)) if packed and rng.random() < 0.8 else N for _ in range(B)]
+    schedule = ["auto", "full", "symmetric", "full_64"][rng.integers(0, 4)]
+    return rng, dtype, D, B, N, packed, ns, schedule
+
+
+@pytest.mark.parametrize("seed", range(64))
+def test_random_configurations(seed):
+    """64 seeded configurations (_random_config): two insertions, composition and
+    gather, every image checked stage by stage against the oracle and through the
+    reconstruction."""
+    rng, dtype, D, B, N, packed, ns, schedule = _random_config(seed)
+    print(f"random config {seed}: {dtype} D={D} B={B} N={N} packed={packed} sizes={ns} schedule={schedule}",
+          flush=True)
+    imgs = [store(clustered(rng, n, D, k=max(1, n // int(rng.integers(2, 9)))), dtype) for n in ns]
+    if packed:
+        x = torch.cat(imgs).to(DEV)
+        off = torch.tensor(np.concatenate([[0], np.cumsum(ns)]), dtype=torch.int32, device=DEV)
+    else:
+        x, off = torch.stack(imgs).to(DEV), None
+    m1 = mpm.merge(x, off, N=N, schedule=schedule)
+    m2 = mpm.merge(m1.y, m1.y_off, N=N, schedule=schedule)
+    out, rstar = mpm.compose_unmerge(m2.y, m2.y_off, m1.map, m2.map)
+    torch.cuda.synchronize()
+    o1, o2 = m1.y_off.cpu().numpy(), m2.y_off.cpu().numpy()
+    nb1, nb2 = m1.nb.cpu().numpy(), m2.nb.cpu().numpy()
+    map1, map2, rs = m1.map.cpu().numpy(), m2.map.cpu().numpy(), rstar.cpu().numpy()
+    y1, y2 = to64(m1.y[: o1[-1]]), to64(m2.y[: o2[-1]])
+    up = to64(out)
+    for b, n in enumerate(ns):
+        if n == 0:
+            assert o1[b + 1] == o1[b] and o2[b + 1] == o2[b] and np.all(rs[b] == -1) and not up[b].any(), b
+            continue
+        s1 = check_stage(to64(imgs[b]), dtype, nb1[b, :n], map1[b], y1[o1[b]:o1[b + 1]])
+        check_stage(y1[o1[b]:o1[b + 1]], dtype, nb2[b, :s1.count], map2[b], y2[o2[b]:o2[b + 1]])
+        r = oracle.compose(map1[b, :n], map2[b, :s1.count])
+        assert np.array_equal(rs[b, :n], r) and np.all(rs[b, n:] == -1), f"image {b}: composed map"
+        assert np.array_equal(up[b, :n], oracle.unmerge(y2[o2[b]:o2[b + 1]], r)), f"image {b}: gather"
+        assert not up[b, n:].any(), f"image {b}: rows past n_b"
+
+
 # ---- empty images in a packed batch --------------------------------------------------
 
 _EMPTY_SIZES = [0, 5, 0, 300, 1, 0, 257, 2, 0, 600]
